@@ -1,0 +1,114 @@
+// Shared device types, small helpers and the launcher declarations of the
+// Encode-stage encoder kernels (gfx950 / CDNA4).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+typedef __bf16 bf16;
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 bf16x4;
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
+
+namespace eas {
+
+constexpr int kMaxSeqs = 64;
+
+// Per-micro-batch sequence metadata, passed to kernels by value.
+struct SeqMeta {
+  int n;                    // sequences
+  int cls;                  // 1 if every sequence starts with a CLS token
+  int merge;                // 1 or 2
+  int cu[kMaxSeqs + 1];     // token prefix sums
+  int thw[kMaxSeqs][3];     // patch grid per sequence
+};
+
+// Attention work list: q-tiles of all sequences, longest sequence first.
+struct AttnWork {
+  int n;                    // sequences
+  int cu[kMaxSeqs + 1];
+  int order[kMaxSeqs];      // order[i] = sequence handled by the i-th tile group
+  int tile_start[kMaxSeqs + 1];  // prefix sums of q-tiles over `order`
+};
+
+enum Act { ACT_NONE = 0, ACT_GELU = 1, ACT_QUICKGELU = 2 };
+
+__device__ __forceinline__ float gelu_erf(float v) { return 0.5f * v * (1.0f + erff(v * 0.70710678118654752f)); }
+__device__ __forceinline__ float quick_gelu(float v) { return v / (1.0f + __expf(-1.702f * v)); }
+__device__ __forceinline__ float apply_act(int act, float v) {
+  if (act == ACT_GELU) return gelu_erf(v);
+  if (act == ACT_QUICKGELU) return quick_gelu(v);
+  return v;
+}
+
+template <class T> __device__ __forceinline__ float to_f(T v) { return (float)v; }
+template <class T> __device__ __forceinline__ T from_f(float v) { return (T)v; }
+
+// Row r's sequence: largest s with cu[s] <= r.
+__device__ __forceinline__ int find_seq(const int* cu, int n, int r) {
+  int lo = 0, hi = n - 1;
+  while (lo < hi) {
+    int mid = (lo + hi + 1) >> 1;
+    if (cu[mid] <= r) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+// Fused GEMM epilogue / prologue description:
+//   out[m, n] = act(sum_k A'[m, k] * B[n, k] + bias[n]) + pos[idx(m), n] + resid[m, n]
+// where A' is A itself, or LayerNorm(A) when `stats` is set:
+//   A'[m, k] = (A[m, k] - mu[t]) * rstd[t] * g[k % ln_dim] + b[k % ln_dim],
+//   t = m * ln_group + k / ln_dim   (ln_group = 4 views 4 tokens as one row).
+struct GemmArgs {
+  int M, N, K;
+  const void* A; int lda;          // [M, lda]: model dtype, or fp32 when stats != null
+  const void* B; int ldb;          // [N, ldb] model dtype
+  const float2* stats;             // per token (mean, rstd) or null
+  const void* ln_g; const void* ln_b; int ln_dim; int ln_group;
+  const void* bias;                // [N] model dtype or null
+  int act;
+  const void* pos; int pos_f32; int ld_pos;   // position table (model dtype or fp32)
+  const int* pos_idx; int pos_period;         // table row: pos_idx[m] or m % pos_period
+  const float* resid; int ldr;                // fp32 residual (may alias out)
+  void* out; int ldo; int out_f32;
+};
+
+// ---- launchers (each returns hipGetLastError() of its launch) --------------
+hipError_t launch_gemm_bf16(const GemmArgs& a, hipStream_t s, const char** kname);
+hipError_t launch_gemm_f32(const GemmArgs& a, hipStream_t s, const char** kname);
+
+struct AttnArgs {
+  const void* qkv; int ldqkv;      // [N, ldqkv]: q | k | v blocks of width heads*hd
+  void* out; int ldo;              // [N, ldo]
+  int heads, hd;
+  float scale;                     // 1 / sqrt(hd)
+};
+hipError_t launch_attention_bf16(const AttnArgs& a, const AttnWork& w, int total_tiles, hipStream_t s,
+                                 const char** kname);
+hipError_t launch_attention_f32(const AttnArgs& a, const AttnWork& w, int total_tiles, hipStream_t s,
+                                const char** kname);
+int attention_q_tile(int dtype_bf16);
+
+hipError_t launch_positions(const SeqMeta& m, int N, int4* pos3, int* tab_idx, int pos_gw, hipStream_t s);
+hipError_t launch_ln_stats(const float* x, int N, int d, float eps, float2* stats, hipStream_t s);
+hipError_t launch_ln_apply(const float* x, int N, int d, float eps, const void* g, const void* b, int w_bf16,
+                           void* y, int y_f32, hipStream_t s);
+hipError_t launch_rope(void* qkv, int ldqkv, int N, int heads, int hd, int is_bf16, const int4* pos3,
+                       const float* inv_freq, const int* slot_axis, hipStream_t s);
+hipError_t launch_cls(const SeqMeta& m, float* x, int d, const void* cls, const void* pos0, int w_bf16,
+                      hipStream_t s);
+hipError_t launch_im2col_k3(const void* src, int frames_in, int C, int n_clips, int stride, int is_bf16,
+                            void* dst, hipStream_t s);
+
+struct PackArgs {
+  int n;
+  int cu[kMaxSeqs + 1];
+  int tchw[kMaxSeqs][4];
+  const float* src[kMaxSeqs];
+};
+hipError_t launch_pack_vision(const PackArgs& p, int cls, int merge, int patch, int tp, int K, int is_bf16,
+                              void* packed, long total, hipStream_t s);
+hipError_t launch_pack_audio(const PackArgs& p, int n_mels, int n_frames, int is_bf16, void* packed,
+                             hipStream_t s);
+
+}  // namespace eas

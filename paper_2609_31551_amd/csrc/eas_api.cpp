@@ -1,0 +1,757 @@
+// Host side of libeas.so: the C ABI declared in include/eas_encoder.h.
+//
+// eas_encode_microbatch runs the Encode forward pass (paper Section 2.1) on
+// one padding-free micro-batch (Section 3.2) as a fixed sequence of kernel
+// launches on the caller's stream:
+//   embed (patch GEMM + positions [+ CLS, ln_pre] | conv1d x2 + sinusoid)
+//   per layer: LN1 stats -> QKV GEMM (LN prologue) [-> RoPE] -> attention
+//              -> O GEMM (+residual) -> LN2 stats -> FC1 GEMM (LN prologue, act)
+//              -> FC2 GEMM (+residual)
+//   connector: merger (LN stats -> GEMM+GELU with LN prologue -> GEMM) | ln_post | none
+// Every per-call shape fact travels to the kernels by value (SeqMeta,
+// AttnWork), so a call needs no host-to-device copies and no device sync.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/eas_encoder.h"
+#include "common.h"
+
+using namespace eas;
+
+namespace {
+
+struct TensorDesc {
+  std::string name;
+  int64_t offset;
+  int ndim;
+  int64_t shape[2];
+  int64_t numel() const { return ndim == 1 ? shape[0] : shape[0] * shape[1]; }
+};
+
+struct Layout {
+  std::vector<TensorDesc> t;
+  int64_t total = 0;
+  int64_t elem = 2;
+  void add(const std::string& name, int64_t s0, int64_t s1 = -1) {
+    TensorDesc d;
+    d.name = name;
+    d.ndim = s1 < 0 ? 1 : 2;
+    d.shape[0] = s0;
+    d.shape[1] = s1 < 0 ? 0 : s1;
+    d.offset = total;
+    total += (d.numel() * elem + 255) / 256 * 256;
+    t.push_back(d);
+  }
+  int64_t off(const std::string& name) const {
+    for (const auto& d : t)
+      if (d.name == name) return d.offset;
+    return -1;
+  }
+};
+
+int64_t k_patch(const eas_config& c) {
+  if (c.kind == EAS_KIND_WHISPER) return c.n_mels;
+  return (int64_t)c.in_chans * c.temporal_patch * c.patch * c.patch;
+}
+
+Layout build_layout(const eas_config& c) {
+  Layout L;
+  L.elem = c.dtype == EAS_BF16 ? 2 : 4;
+  const int64_t d = c.hidden, f = c.mlp;
+  if (c.kind == EAS_KIND_WHISPER) {
+    L.add("conv1.w", d, (int64_t)c.n_mels * 3);
+    L.add("conv1.b", d);
+    L.add("conv2.w", d, d * 3);
+    L.add("conv2.b", d);
+  } else {
+    L.add("patch.w", d, k_patch(c));
+    L.add("patch.b", d);
+  }
+  const int64_t gh = c.pos_grid[0], gw = c.pos_grid[1];
+  if (c.kind == EAS_KIND_VIT_CLS_ABS) {
+    L.add("cls", d);
+    L.add("pos", 1 + gh * gw, d);
+    L.add("ln_pre.g", d);
+    L.add("ln_pre.b", d);
+  } else if (c.kind == EAS_KIND_VIT_ABS) {
+    L.add("pos", gh * gw, d);
+  }
+  for (int i = 0; i < c.layers; ++i) {
+    const std::string p = "layers." + std::to_string(i) + ".";
+    L.add(p + "ln1.g", d);
+    L.add(p + "ln1.b", d);
+    L.add(p + "qkv.w", 3 * d, d);
+    L.add(p + "qkv.b", 3 * d);
+    L.add(p + "o.w", d, d);
+    L.add(p + "o.b", d);
+    L.add(p + "ln2.g", d);
+    L.add(p + "ln2.b", d);
+    L.add(p + "fc1.w", f, d);
+    L.add(p + "fc1.b", f);
+    L.add(p + "fc2.w", d, f);
+    L.add(p + "fc2.b", d);
+  }
+  if (c.merge == 2) {
+    L.add("ln_q.g", d);
+    L.add("ln_q.b", d);
+    L.add("m1.w", 4 * d, 4 * d);
+    L.add("m1.b", 4 * d);
+    L.add("m2.w", c.out_dim, 4 * d);
+    L.add("m2.b", c.out_dim);
+  }
+  if (c.kind == EAS_KIND_WHISPER) {
+    L.add("ln_post.g", d);
+    L.add("ln_post.b", d);
+  }
+  return L;
+}
+
+// Returns "" when the config is usable, else the reason.
+std::string check_config(const eas_config& c, eas_status* st) {
+  *st = EAS_ERR_INVALID_ARG;
+  if (c.kind < EAS_KIND_VIT_ABS || c.kind > EAS_KIND_WHISPER) return "unknown kind";
+  if (c.dtype != EAS_FP32 && c.dtype != EAS_BF16) return "dtype must be EAS_FP32 or EAS_BF16";
+  if (c.out_dtype != EAS_FP32 && c.out_dtype != EAS_BF16) return "out_dtype must be EAS_FP32 or EAS_BF16";
+  if (c.act != EAS_ACT_GELU && c.act != EAS_ACT_QUICKGELU) return "unknown act";
+  if (c.layers < 0 || c.hidden <= 0 || c.heads <= 0 || c.head_dim <= 0 || c.mlp <= 0) return "non-positive width";
+  if (c.heads * c.head_dim != c.hidden) return "heads * head_dim != hidden";
+  if (c.merge != 1 && c.merge != 2) return "merge must be 1 or 2";
+  if (c.merge == 2 && c.kind != EAS_KIND_VIT_ABS && c.kind != EAS_KIND_VIT_ROPE) return "merger needs a ViT kind";
+  if (c.merge == 2 && c.out_dim <= 0) return "out_dim must be positive with the merger";
+  if (c.merge == 1 && c.out_dim != c.hidden) return "out_dim must equal hidden without a merger";
+  if (c.max_tokens <= 0 || c.max_tokens > (1L << 30)) return "max_tokens out of range";
+  if (c.max_seqs <= 0 || c.max_seqs > EAS_MAX_SEQS) return "max_seqs out of range";
+  if (!(c.ln_eps > 0.0f) || !(c.merger_ln_eps > 0.0f)) return "LayerNorm eps must be positive";
+  if (c.kind == EAS_KIND_WHISPER) {
+    if (c.n_mels <= 0 || c.n_frames <= 0 || c.n_frames % 2) return "n_mels / n_frames invalid";
+  } else {
+    if (c.in_chans <= 0 || c.patch <= 0 || c.temporal_patch <= 0) return "patch geometry invalid";
+  }
+  if ((c.kind == EAS_KIND_VIT_ABS || c.kind == EAS_KIND_VIT_CLS_ABS) && (c.pos_grid[0] <= 0 || c.pos_grid[1] <= 0))
+    return "pos_grid must be positive";
+  if (c.kind == EAS_KIND_VIT_ROPE) {
+    if (c.head_dim % 2) return "head_dim must be even for RoPE";
+    int s = 0;
+    for (int i = 0; i < 3; ++i) {
+      if (c.rope_sections[i] < 0) return "negative rope section";
+      s += c.rope_sections[i];
+    }
+    if (s != c.head_dim / 2) return "rope_sections must sum to head_dim / 2";
+    if (!(c.rope_theta > 0.0f)) return "rope_theta must be positive";
+  }
+  *st = EAS_ERR_UNSUPPORTED;
+  if (c.hidden % 8 || c.mlp % 8 || (c.merge == 2 && c.out_dim % 8)) return "widths must be multiples of 8";
+  if (c.hidden > 2048) return "hidden above 2048 is not built";
+  if (c.dtype == EAS_BF16 && c.head_dim != 16 && c.head_dim != 32 && c.head_dim != 64 && c.head_dim != 80 &&
+      c.head_dim != 128)
+    return "bf16 head_dim must be 16, 32, 64, 80 or 128";
+  if (c.dtype == EAS_FP32 && c.head_dim != 16 && c.head_dim != 32 && c.head_dim != 64 && c.head_dim != 80)
+    return "fp32 head_dim must be 16, 32, 64 or 80";
+  *st = EAS_OK;
+  return "";
+}
+
+// Token count of a request from its input shape (frames, C, H, W); -1 if invalid.
+int64_t request_tokens(const eas_config& c, const int32_t* tchw, int32_t* grid, std::string* why) {
+  if (c.kind == EAS_KIND_WHISPER) {
+    if (tchw[0] != 1 || tchw[1] != 1 || tchw[2] != c.n_mels || tchw[3] != c.n_frames) {
+      *why = "audio items must be (1, 1, n_mels, n_frames)";
+      return -1;
+    }
+    if (grid) grid[0] = 1, grid[1] = 1, grid[2] = c.n_frames / 2;
+    return c.n_frames / 2;
+  }
+  const int T = tchw[0], C = tchw[1], H = tchw[2], W = tchw[3];
+  if (C != c.in_chans || T <= 0 || H <= 0 || W <= 0 || T % c.temporal_patch || H % c.patch || W % c.patch) {
+    *why = "item does not tile into patches";
+    return -1;
+  }
+  const int t = T / c.temporal_patch, h = H / c.patch, w = W / c.patch;
+  if (grid) grid[0] = t, grid[1] = h, grid[2] = w;
+  return (int64_t)t * h * w + (c.kind == EAS_KIND_VIT_CLS_ABS ? 1 : 0);
+}
+
+std::string check_batch(const eas_config& c, const int32_t* cu, const int32_t* grid, int32_t n, eas_status* st) {
+  *st = EAS_ERR_INVALID_ARG;
+  if (!cu) return "cu_seqlens is NULL";
+  if (!grid && c.kind != EAS_KIND_WHISPER) return "grid_thw is NULL";
+  *st = EAS_ERR_CAPACITY;
+  if (n < 1 || n > c.max_seqs) return "n_seqs outside 1..max_seqs";
+  *st = EAS_ERR_SHAPE;
+  if (cu[0] != 0) return "cu_seqlens[0] != 0";
+  for (int r = 0; r < n; ++r) {
+    if (cu[r + 1] <= cu[r]) return "cu_seqlens not strictly increasing";
+    const int64_t L = cu[r + 1] - cu[r];
+    if (c.kind == EAS_KIND_WHISPER) {
+      if (L != c.n_frames / 2) return "audio sequence length != n_frames / 2";
+      continue;
+    }
+    const int t = grid[3 * r], h = grid[3 * r + 1], w = grid[3 * r + 2];
+    if (t <= 0 || h <= 0 || w <= 0) return "grid_thw entries must be positive";
+    const int64_t want = (int64_t)t * h * w + (c.kind == EAS_KIND_VIT_CLS_ABS ? 1 : 0);
+    if (L != want) return "sequence length does not match grid_thw";
+    if (c.merge == 2 && (h % 2 || w % 2)) return "2x2 merger needs even h and w";
+    if ((c.kind == EAS_KIND_VIT_ABS || c.kind == EAS_KIND_VIT_CLS_ABS) &&
+        (t != 1 || h > c.pos_grid[0] || w > c.pos_grid[1]))
+      return "patch grid does not fit the position table";
+  }
+  *st = EAS_ERR_CAPACITY;
+  if (cu[n] > c.max_tokens) return "more tokens than max_tokens";
+  *st = EAS_OK;
+  return "";
+}
+
+struct ProfRec {
+  const char* kernel;
+  hipEvent_t e0, e1;
+  double flops, bytes;
+};
+
+}  // namespace
+
+struct eas_encoder {
+  eas_config cfg;
+  Layout layout;
+  int device = 0;
+  char* ws = nullptr;
+  float* x = nullptr;        // residual stream [max_tokens, d] fp32
+  float2* stats = nullptr;   // (mean, rstd) per token
+  void* qkv = nullptr;       // [max_tokens, 3d]
+  void* ao = nullptr;        // attention output [max_tokens, d]
+  void* hbuf = nullptr;      // MLP hidden [max_tokens, max(f, 4d, 3d)]
+  int4* pos3 = nullptr;      // (t, h, w) per token
+  int* tab_idx = nullptr;    // learned-position row per token
+  float* sinus = nullptr;    // [n_frames/2, d] (WHISPER)
+  float* inv_freq = nullptr; // [head_dim/2] (VIT_ROPE)
+  int* slot_axis = nullptr;  // [head_dim/2]
+  std::string err;
+  bool prof = false;
+  std::vector<ProfRec> recs;
+  std::vector<hipEvent_t> pool;
+};
+
+namespace {
+
+eas_status fail(eas_encoder* e, eas_status s, const std::string& msg) {
+  if (e) e->err = msg;
+  return s;
+}
+
+hipEvent_t get_event(eas_encoder* e) {
+  if (!e->pool.empty()) {
+    hipEvent_t ev = e->pool.back();
+    e->pool.pop_back();
+    return ev;
+  }
+  hipEvent_t ev = nullptr;
+  if (hipEventCreate(&ev) != hipSuccess) return nullptr;
+  return ev;
+}
+
+// Runs one launch, bracketed by events while profiling is on.
+template <class F>
+eas_status run(eas_encoder* e, hipStream_t s, double flops, double bytes, F&& launch) {
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (e->prof) {
+    e0 = get_event(e);
+    e1 = get_event(e);
+    if (e0) (void)hipEventRecord(e0, s);
+  }
+  const char* kname = "unnamed";
+  const hipError_t err = launch(&kname);
+  if (e->prof && e0 && e1) {
+    (void)hipEventRecord(e1, s);
+    e->recs.push_back({kname, e0, e1, flops, bytes});
+  }
+  if (err != hipSuccess) return fail(e, EAS_ERR_HIP, std::string(kname) + ": " + hipGetErrorString(err));
+  return EAS_OK;
+}
+
+GemmArgs gemm_args(int M, int N, int K, const void* A, int lda, const void* B, int ldb, void* out, int ldo,
+                   int out_f32) {
+  GemmArgs g;
+  std::memset(&g, 0, sizeof(g));
+  g.M = M; g.N = N; g.K = K;
+  g.A = A; g.lda = lda;
+  g.B = B; g.ldb = ldb;
+  g.out = out; g.ldo = ldo; g.out_f32 = out_f32;
+  g.ln_group = 1;
+  g.pos_period = 1;
+  return g;
+}
+
+eas_status gemm(eas_encoder* e, const GemmArgs& g, hipStream_t s) {
+  const bool bf = e->cfg.dtype == EAS_BF16;
+  const double el = bf ? 2.0 : 4.0;
+  const double flops = 2.0 * g.M * g.N * (double)g.K;
+  double bytes = (double)g.M * g.K * (g.stats ? 4.0 : el) + (double)g.N * g.K * el + (double)g.M * g.N * (g.out_f32 ? 4.0 : el);
+  if (g.resid) bytes += (double)g.M * g.N * 4.0;
+  return run(e, s, flops, bytes, [&](const char** kn) {
+    return bf ? launch_gemm_bf16(g, s, kn) : launch_gemm_f32(g, s, kn);
+  });
+}
+
+const char* wptr(const void* weights, const eas_encoder* e, const std::string& name) {
+  const int64_t off = e->layout.off(name);
+  return off < 0 ? nullptr : static_cast<const char*>(weights) + off;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* eas_status_string(eas_status s) {
+  switch (s) {
+    case EAS_OK: return "ok";
+    case EAS_ERR_INVALID_ARG: return "invalid argument";
+    case EAS_ERR_SHAPE: return "shape error";
+    case EAS_ERR_CAPACITY: return "capacity exceeded";
+    case EAS_ERR_UNSUPPORTED: return "unsupported configuration";
+    case EAS_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+const char* eas_last_error(const eas_encoder* enc) { return enc ? enc->err.c_str() : ""; }
+
+eas_status eas_weights_layout(const eas_config* cfg, eas_tensor_desc* descs, int32_t capacity, int32_t* n_descs,
+                              int64_t* total_bytes) {
+  if (!cfg || !n_descs) return EAS_ERR_INVALID_ARG;
+  eas_status st;
+  if (!check_config(*cfg, &st).empty()) return st;
+  const Layout L = build_layout(*cfg);
+  *n_descs = (int32_t)L.t.size();
+  if (total_bytes) *total_bytes = L.total;
+  if (!descs) return EAS_OK;
+  if (capacity < (int32_t)L.t.size()) return EAS_ERR_CAPACITY;
+  for (size_t i = 0; i < L.t.size(); ++i) {
+    std::memset(&descs[i], 0, sizeof(eas_tensor_desc));
+    std::snprintf(descs[i].name, sizeof(descs[i].name), "%s", L.t[i].name.c_str());
+    descs[i].offset_bytes = L.t[i].offset;
+    descs[i].ndim = L.t[i].ndim;
+    descs[i].shape[0] = L.t[i].shape[0];
+    descs[i].shape[1] = L.t[i].shape[1];
+  }
+  return EAS_OK;
+}
+
+eas_status eas_microbatch_shape(const eas_config* cfg, int32_t n_req, const int32_t* tchw, int32_t* cu_seqlens,
+                                int32_t* grid_thw, int64_t* packed_elems, int64_t* out_rows) {
+  if (!cfg || !tchw || !cu_seqlens) return EAS_ERR_INVALID_ARG;
+  eas_status st;
+  if (!check_config(*cfg, &st).empty()) return st;
+  if (n_req < 1 || n_req > cfg->max_seqs) return EAS_ERR_CAPACITY;
+  std::string why;
+  int64_t tot = 0;
+  cu_seqlens[0] = 0;
+  for (int r = 0; r < n_req; ++r) {
+    int32_t g[3];
+    const int64_t L = request_tokens(*cfg, tchw + 4 * r, g, &why);
+    if (L < 0) return EAS_ERR_SHAPE;
+    if (cfg->merge == 2 && (g[1] % 2 || g[2] % 2)) return EAS_ERR_SHAPE;
+    tot += L;
+    if (tot > cfg->max_tokens) return EAS_ERR_CAPACITY;
+    cu_seqlens[r + 1] = (int32_t)tot;
+    if (grid_thw) std::memcpy(grid_thw + 3 * r, g, sizeof(g));
+  }
+  if (packed_elems) *packed_elems = cfg->kind == EAS_KIND_WHISPER ? (int64_t)n_req * cfg->n_mels * cfg->n_frames
+                                                                   : tot * k_patch(*cfg);
+  if (out_rows) *out_rows = cfg->merge == 2 ? tot / 4 : tot;
+  return EAS_OK;
+}
+
+eas_status eas_validate_microbatch(const eas_config* cfg, const int32_t* cu_seqlens, const int32_t* grid_thw,
+                                   int32_t n_seqs) {
+  if (!cfg) return EAS_ERR_INVALID_ARG;
+  eas_status st;
+  if (!check_config(*cfg, &st).empty()) return st;
+  check_batch(*cfg, cu_seqlens, grid_thw, n_seqs, &st);
+  return st;
+}
+
+eas_status eas_encoder_create(const eas_config* cfg, eas_encoder** out) {
+  if (!cfg || !out) return EAS_ERR_INVALID_ARG;
+  *out = nullptr;
+  eas_status st;
+  const std::string why = check_config(*cfg, &st);
+  if (!why.empty()) return st;
+  eas_encoder* e = new (std::nothrow) eas_encoder();
+  if (!e) return EAS_ERR_HIP;
+  e->cfg = *cfg;
+  e->layout = build_layout(*cfg);
+  if (hipGetDevice(&e->device) != hipSuccess) {
+    delete e;
+    return EAS_ERR_HIP;
+  }
+  const eas_config& c = *cfg;
+  const int64_t N = c.max_tokens, d = c.hidden, el = c.dtype == EAS_BF16 ? 2 : 4;
+  const int64_t hw = std::max<int64_t>({c.mlp, 4 * d, 3 * d});
+  int64_t qkv_rows = N, ao_rows = N;
+  if (c.kind == EAS_KIND_WHISPER) {   // front-end im2col and conv1 output reuse qkv / ao
+    qkv_rows = std::max<int64_t>(N, (2 * N * d + 3 * d - 1) / (3 * d));
+    ao_rows = std::max<int64_t>(N, (2 * N * 3 * c.n_mels + d - 1) / d);
+  }
+  auto al = [](int64_t b) { return (b + 255) / 256 * 256; };
+  const int64_t half = d / c.heads / 2;
+  int64_t sz[9] = {al(N * d * 4), al(N * 8), al(qkv_rows * 3 * d * el), al(ao_rows * d * el), al(N * hw * el),
+                   al(N * 16), al(N * 4), al(c.kind == EAS_KIND_WHISPER ? (int64_t)c.n_frames / 2 * d * 4 : 256),
+                   al(half * 8 + 256)};
+  int64_t total = 0;
+  for (int64_t v : sz) total += v;
+  if (hipMalloc(&e->ws, total) != hipSuccess) {
+    delete e;
+    return EAS_ERR_HIP;
+  }
+  char* p = e->ws;
+  e->x = (float*)p; p += sz[0];
+  e->stats = (float2*)p; p += sz[1];
+  e->qkv = p; p += sz[2];
+  e->ao = p; p += sz[3];
+  e->hbuf = p; p += sz[4];
+  e->pos3 = (int4*)p; p += sz[5];
+  e->tab_idx = (int*)p; p += sz[6];
+  e->sinus = (float*)p; p += sz[7];
+  e->inv_freq = (float*)p;
+  e->slot_axis = (int*)(p + al(half * 4));
+  hipError_t herr = hipSuccess;
+  if (c.kind == EAS_KIND_WHISPER) {   // Whisper-style sinusoid table, computed in double
+    const int64_t F = c.n_frames / 2, hc = d / 2;
+    std::vector<float> tab(F * d);
+    const double inc = std::log(10000.0) / (double)(hc - 1);
+    for (int64_t t = 0; t < F; ++t)
+      for (int64_t i = 0; i < hc; ++i) {
+        const double a = (double)t * std::exp(-inc * (double)i);
+        tab[t * d + i] = (float)std::sin(a);
+        tab[t * d + hc + i] = (float)std::cos(a);
+      }
+    herr = hipMemcpy(e->sinus, tab.data(), tab.size() * 4, hipMemcpyHostToDevice);
+  }
+  if (c.kind == EAS_KIND_VIT_ROPE && herr == hipSuccess) {   // slot k of axis a turns by theta^(-j / n_a)
+    std::vector<float> inv;
+    std::vector<int> ax;
+    for (int a = 0; a < 3; ++a)
+      for (int j = 0; j < c.rope_sections[a]; ++j) {
+        inv.push_back((float)std::pow((double)c.rope_theta, -(double)j / (double)c.rope_sections[a]));
+        ax.push_back(a);
+      }
+    herr = hipMemcpy(e->inv_freq, inv.data(), inv.size() * 4, hipMemcpyHostToDevice);
+    if (herr == hipSuccess) herr = hipMemcpy(e->slot_axis, ax.data(), ax.size() * 4, hipMemcpyHostToDevice);
+  }
+  if (herr != hipSuccess) {
+    (void)hipFree(e->ws);
+    delete e;
+    return EAS_ERR_HIP;
+  }
+  *out = e;
+  return EAS_OK;
+}
+
+void eas_encoder_destroy(eas_encoder* enc) {
+  if (!enc) return;
+  (void)hipDeviceSynchronize();
+  for (auto& r : enc->recs) {
+    (void)hipEventDestroy(r.e0);
+    (void)hipEventDestroy(r.e1);
+  }
+  for (auto ev : enc->pool) (void)hipEventDestroy(ev);
+  (void)hipFree(enc->ws);
+  delete enc;
+}
+
+eas_status eas_profile_enable(eas_encoder* enc, int32_t enable) {
+  if (!enc) return EAS_ERR_INVALID_ARG;
+  enc->prof = enable != 0;
+  return EAS_OK;
+}
+
+eas_status eas_profile_read(eas_encoder* enc, eas_kernel_stat* stats, int32_t capacity, int32_t* n_stats) {
+  if (!enc || !n_stats) return EAS_ERR_INVALID_ARG;
+  std::vector<eas_kernel_stat> agg;
+  for (auto& r : enc->recs) {
+    if (hipEventSynchronize(r.e1) != hipSuccess) return fail(enc, EAS_ERR_HIP, "hipEventSynchronize failed");
+    float ms = 0.0f;
+    (void)hipEventElapsedTime(&ms, r.e0, r.e1);
+    eas_kernel_stat* k = nullptr;
+    for (auto& a : agg)
+      if (std::strcmp(a.kernel, r.kernel) == 0) k = &a;
+    if (!k) {
+      agg.push_back(eas_kernel_stat());
+      k = &agg.back();
+      std::memset(k, 0, sizeof(*k));
+      std::snprintf(k->kernel, sizeof(k->kernel), "%s", r.kernel);
+    }
+    k->launches += 1;
+    k->total_ms += ms;
+    k->flops += r.flops;
+    k->bytes += r.bytes;
+  }
+  *n_stats = (int32_t)agg.size();
+  if (!stats) return EAS_OK;
+  for (auto& r : enc->recs) {
+    enc->pool.push_back(r.e0);
+    enc->pool.push_back(r.e1);
+  }
+  enc->recs.clear();
+  for (int32_t i = 0; i < std::min<int32_t>(capacity, (int32_t)agg.size()); ++i) stats[i] = agg[i];
+  return capacity < (int32_t)agg.size() ? EAS_ERR_CAPACITY : EAS_OK;
+}
+
+eas_status eas_pack_microbatch(eas_encoder* enc, int32_t n_req, const float* const* items, const int32_t* tchw,
+                               void* packed, int32_t* cu_seqlens, int32_t* grid_thw, void* stream) {
+  if (!enc || !items || !tchw || !packed || !cu_seqlens) return fail(enc, EAS_ERR_INVALID_ARG, "NULL argument");
+  const eas_config& c = enc->cfg;
+  int32_t cu[EAS_MAX_SEQS + 1], grid[EAS_MAX_SEQS * 3];
+  int64_t elems = 0;
+  if (n_req < 1 || n_req > c.max_seqs) return fail(enc, EAS_ERR_CAPACITY, "n_req outside 1..max_seqs");
+  const eas_status st = eas_microbatch_shape(&c, n_req, tchw, cu, grid, &elems, nullptr);
+  if (st != EAS_OK) return fail(enc, st, "item shapes rejected");
+  for (int r = 0; r < n_req; ++r)
+    if (!items[r]) return fail(enc, EAS_ERR_INVALID_ARG, "NULL item pointer");
+  PackArgs p;
+  std::memset(&p, 0, sizeof(p));
+  p.n = n_req;
+  for (int r = 0; r <= n_req; ++r) p.cu[r] = cu[r];
+  for (int r = 0; r < n_req; ++r) {
+    for (int k = 0; k < 4; ++k) p.tchw[r][k] = tchw[4 * r + k];
+    p.src[r] = items[r];
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int bf = c.dtype == EAS_BF16;
+  const eas_status rs = run(enc, s, 0.0, (double)elems * (4 + (bf ? 2 : 4)), [&](const char** kn) {
+    if (c.kind == EAS_KIND_WHISPER) {
+      *kn = "pack_audio";
+      return launch_pack_audio(p, c.n_mels, c.n_frames, bf, packed, s);
+    }
+    *kn = "pack_vision";
+    return launch_pack_vision(p, c.kind == EAS_KIND_VIT_CLS_ABS, c.merge, c.patch, c.temporal_patch,
+                              (int)k_patch(c), bf, packed, elems, s);
+  });
+  if (rs != EAS_OK) return rs;
+  std::memcpy(cu_seqlens, cu, sizeof(int32_t) * (n_req + 1));
+  if (grid_thw) std::memcpy(grid_thw, grid, sizeof(int32_t) * 3 * n_req);
+  return EAS_OK;
+}
+
+eas_status eas_encode_microbatch(eas_encoder* enc, const void* packed_in, const int32_t* cu_seqlens,
+                                 const int32_t* grid_thw, int32_t n_seqs, const void* weights, void* out_embeddings,
+                                 int32_t* cu_out, void* stream) {
+  if (!enc) return EAS_ERR_INVALID_ARG;
+  if (!packed_in || !weights || !out_embeddings) return fail(enc, EAS_ERR_INVALID_ARG, "NULL device pointer");
+  const eas_config& c = enc->cfg;
+  eas_status st;
+  const std::string why = check_batch(c, cu_seqlens, grid_thw, n_seqs, &st);
+  if (st != EAS_OK) return fail(enc, st, why);
+  if (c.kind == EAS_KIND_VIT_CLS_ABS && c.layers == 0 && c.out_dtype != EAS_FP32)
+    return fail(enc, EAS_ERR_UNSUPPORTED, "zero-layer CLS model needs fp32 output");
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev != enc->device)
+    return fail(enc, EAS_ERR_INVALID_ARG, "current device differs from the handle's device");
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const bool bf = c.dtype == EAS_BF16;
+  const int out_f32 = c.out_dtype == EAS_FP32;
+  const int N = cu_seqlens[n_seqs], d = c.hidden, f = c.mlp, H = c.heads, hd = c.head_dim;
+  const int d3 = 3 * d;
+  const int64_t el = bf ? 2 : 4;
+
+  SeqMeta meta;
+  std::memset(&meta, 0, sizeof(meta));
+  meta.n = n_seqs;
+  meta.cls = c.kind == EAS_KIND_VIT_CLS_ABS;
+  meta.merge = c.merge;
+  for (int r = 0; r <= n_seqs; ++r) meta.cu[r] = cu_seqlens[r];
+  if (grid_thw)
+    for (int r = 0; r < n_seqs; ++r)
+      for (int k = 0; k < 3; ++k) meta.thw[r][k] = grid_thw[3 * r + k];
+
+  // attention work list: longest sequences first
+  AttnWork work;
+  std::memset(&work, 0, sizeof(work));
+  work.n = n_seqs;
+  for (int r = 0; r <= n_seqs; ++r) work.cu[r] = cu_seqlens[r];
+  std::vector<int> ord(n_seqs);
+  for (int r = 0; r < n_seqs; ++r) ord[r] = r;
+  std::stable_sort(ord.begin(), ord.end(), [&](int a, int b) {
+    return cu_seqlens[a + 1] - cu_seqlens[a] > cu_seqlens[b + 1] - cu_seqlens[b];
+  });
+  const int qt = attention_q_tile(bf);
+  int tiles = 0;
+  double attn_flops = 0.0;
+  for (int i = 0; i < n_seqs; ++i) {
+    const int r = ord[i];
+    const int L = cu_seqlens[r + 1] - cu_seqlens[r];
+    work.order[i] = r;
+    work.tile_start[i] = tiles;
+    tiles += (L + qt - 1) / qt;
+    attn_flops += 4.0 * (double)L * L * hd * H;
+  }
+  work.tile_start[n_seqs] = tiles;
+
+  auto W = [&](const std::string& n) { return wptr(weights, enc, n); };
+  eas_status rc = EAS_OK;
+#define EAS_TRY(expr)          \
+  do {                         \
+    rc = (expr);               \
+    if (rc != EAS_OK) return rc; \
+  } while (0)
+
+  const bool vit = c.kind != EAS_KIND_WHISPER;
+  const bool need_pos = vit;
+  if (need_pos)
+    EAS_TRY(run(enc, s, 0.0, (double)N * 20, [&](const char** kn) {
+      *kn = "positions";
+      return launch_positions(meta, N, enc->pos3, enc->tab_idx, c.pos_grid[1], s);
+    }));
+
+  // ---- embedding ----
+  if (vit) {
+    const int K = (int)k_patch(c);
+    GemmArgs g = gemm_args(N, d, K, packed_in, K, W("patch.w"), K, enc->x, d, 1);
+    g.bias = W("patch.b");
+    if (c.kind != EAS_KIND_VIT_ROPE) {
+      g.pos = W("pos");
+      g.pos_f32 = !bf;
+      g.ld_pos = d;
+      g.pos_idx = enc->tab_idx;
+    }
+    EAS_TRY(gemm(enc, g, s));
+    if (c.kind == EAS_KIND_VIT_CLS_ABS) {
+      EAS_TRY(run(enc, s, 0.0, (double)n_seqs * d * 4, [&](const char** kn) {
+        *kn = "cls_insert";
+        return launch_cls(meta, enc->x, d, W("cls"), W("pos"), bf, s);
+      }));
+      EAS_TRY(run(enc, s, 0.0, (double)N * d * 8, [&](const char** kn) {
+        *kn = "ln_apply";
+        return launch_ln_apply(enc->x, N, d, c.ln_eps, W("ln_pre.g"), W("ln_pre.b"), bf, enc->x, 1, s);
+      }));
+    }
+  } else {
+    const int nc = n_seqs, F = c.n_frames, C = c.n_mels;
+    // conv1: im2col [nc*F, 3C] (in ao) -> GEMM + GELU -> [nc*F, d] (in qkv)
+    EAS_TRY(run(enc, s, 0.0, (double)nc * F * C * 3 * el * 2, [&](const char** kn) {
+      *kn = "im2col_k3";
+      return launch_im2col_k3(packed_in, F, C, nc, 1, bf, enc->ao, s);
+    }));
+    GemmArgs g1 = gemm_args(nc * F, d, 3 * C, enc->ao, 3 * C, W("conv1.w"), 3 * C, enc->qkv, d, 0);
+    if (!bf) g1.out_f32 = 1;
+    g1.bias = W("conv1.b");
+    g1.act = ACT_GELU;
+    EAS_TRY(gemm(enc, g1, s));
+    // conv2 (stride 2): im2col [nc*F/2, 3d] (in hbuf) -> GEMM + GELU + sinusoid -> x
+    EAS_TRY(run(enc, s, 0.0, (double)nc * (F / 2) * d * 3 * el * 2, [&](const char** kn) {
+      *kn = "im2col_k3";
+      return launch_im2col_k3(enc->qkv, F, d, nc, 2, bf, enc->hbuf, s);
+    }));
+    GemmArgs g2 = gemm_args(N, d, 3 * d, enc->hbuf, 3 * d, W("conv2.w"), 3 * d, enc->x, d, 1);
+    g2.bias = W("conv2.b");
+    g2.act = ACT_GELU;
+    g2.pos = enc->sinus;
+    g2.pos_f32 = 1;
+    g2.ld_pos = d;
+    g2.pos_period = F / 2;
+    EAS_TRY(gemm(enc, g2, s));
+  }
+
+  // ---- layers ----
+  const int act = c.act == EAS_ACT_GELU ? ACT_GELU : ACT_QUICKGELU;
+  const int mid_f32 = bf ? 0 : 1;   // qkv / attention / MLP activations: model dtype
+  for (int l = 0; l < c.layers; ++l) {
+    const std::string p = "layers." + std::to_string(l) + ".";
+    EAS_TRY(run(enc, s, 0.0, (double)N * (d * 4 + 8), [&](const char** kn) {
+      *kn = "ln_stats";
+      return launch_ln_stats(enc->x, N, d, c.ln_eps, enc->stats, s);
+    }));
+    GemmArgs gq = gemm_args(N, d3, d, enc->x, d, W(p + "qkv.w"), d, enc->qkv, d3, mid_f32);
+    gq.stats = enc->stats;
+    gq.ln_g = W(p + "ln1.g");
+    gq.ln_b = W(p + "ln1.b");
+    gq.ln_dim = d;
+    gq.bias = W(p + "qkv.b");
+    EAS_TRY(gemm(enc, gq, s));
+    if (c.kind == EAS_KIND_VIT_ROPE)
+      EAS_TRY(run(enc, s, 0.0, (double)N * 2 * d * el * 2 + (double)N * 16, [&](const char** kn) {
+        *kn = "rope";
+        return launch_rope(enc->qkv, d3, N, H, hd, bf, enc->pos3, enc->inv_freq, enc->slot_axis, s);
+      }));
+    AttnArgs aa;
+    aa.qkv = enc->qkv;
+    aa.ldqkv = d3;
+    aa.out = enc->ao;
+    aa.ldo = d;
+    aa.heads = H;
+    aa.hd = hd;
+    aa.scale = (float)(1.0 / std::sqrt((double)hd));
+    EAS_TRY(run(enc, s, attn_flops, (double)N * 4 * d * el, [&](const char** kn) {
+      return bf ? launch_attention_bf16(aa, work, tiles, s, kn) : launch_attention_f32(aa, work, tiles, s, kn);
+    }));
+    GemmArgs go = gemm_args(N, d, d, enc->ao, d, W(p + "o.w"), d, enc->x, d, 1);
+    go.bias = W(p + "o.b");
+    go.resid = enc->x;
+    go.ldr = d;
+    EAS_TRY(gemm(enc, go, s));
+    EAS_TRY(run(enc, s, 0.0, (double)N * (d * 4 + 8), [&](const char** kn) {
+      *kn = "ln_stats";
+      return launch_ln_stats(enc->x, N, d, c.ln_eps, enc->stats, s);
+    }));
+    GemmArgs g1 = gemm_args(N, f, d, enc->x, d, W(p + "fc1.w"), d, enc->hbuf, f, mid_f32);
+    g1.stats = enc->stats;
+    g1.ln_g = W(p + "ln2.g");
+    g1.ln_b = W(p + "ln2.b");
+    g1.ln_dim = d;
+    g1.bias = W(p + "fc1.b");
+    g1.act = act;
+    EAS_TRY(gemm(enc, g1, s));
+    // the CLS model's output is the final residual stream: the last FC2 writes it directly
+    const bool direct = c.kind == EAS_KIND_VIT_CLS_ABS && l == c.layers - 1;
+    GemmArgs g2 = gemm_args(N, d, f, enc->hbuf, f, W(p + "fc2.w"), f, direct ? out_embeddings : (void*)enc->x, d,
+                            direct ? out_f32 : 1);
+    g2.bias = W(p + "fc2.b");
+    g2.resid = enc->x;
+    g2.ldr = d;
+    EAS_TRY(gemm(enc, g2, s));
+  }
+
+  // ---- connector ----
+  if (c.merge == 2) {
+    EAS_TRY(run(enc, s, 0.0, (double)N * (d * 4 + 8), [&](const char** kn) {
+      *kn = "ln_stats";
+      return launch_ln_stats(enc->x, N, d, c.merger_ln_eps, enc->stats, s);
+    }));
+    const int G = N / 4, d4 = 4 * d;
+    GemmArgs m1 = gemm_args(G, d4, d4, enc->x, d4, W("m1.w"), d4, enc->hbuf, d4, mid_f32);
+    m1.stats = enc->stats;
+    m1.ln_g = W("ln_q.g");
+    m1.ln_b = W("ln_q.b");
+    m1.ln_dim = d;
+    m1.ln_group = 4;
+    m1.bias = W("m1.b");
+    m1.act = ACT_GELU;
+    EAS_TRY(gemm(enc, m1, s));
+    GemmArgs m2 = gemm_args(G, c.out_dim, d4, enc->hbuf, d4, W("m2.w"), d4, out_embeddings, c.out_dim, out_f32);
+    m2.bias = W("m2.b");
+    EAS_TRY(gemm(enc, m2, s));
+  } else if (c.kind == EAS_KIND_WHISPER) {
+    EAS_TRY(run(enc, s, 0.0, (double)N * d * (4 + (out_f32 ? 4 : 2)), [&](const char** kn) {
+      *kn = "ln_apply";
+      return launch_ln_apply(enc->x, N, d, c.ln_eps, W("ln_post.g"), W("ln_post.b"), bf, out_embeddings, out_f32, s);
+    }));
+  } else if (c.layers == 0) {   // CLS model without layers: the embedding is the output
+    if (hipMemcpyAsync(out_embeddings, enc->x, (size_t)N * d * 4, hipMemcpyDeviceToDevice, s) != hipSuccess)
+      return fail(enc, EAS_ERR_HIP, "hipMemcpyAsync failed");
+  }
+#undef EAS_TRY
+  if (cu_out) {
+    for (int r = 0; r <= n_seqs; ++r) cu_out[r] = c.merge == 2 ? cu_seqlens[r] / 4 : cu_seqlens[r];
+  }
+  enc->err.clear();
+  return EAS_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,265 @@
+// Bandwidth-bound kernels of the Encode path: token positions, LayerNorm
+// statistics / application, rotary position application, CLS insertion,
+// the audio front end's im2col, and the micro-batch packers.
+#include "common.h"
+
+namespace eas {
+namespace {
+
+// (t, h, w) of token j of a t x h x w grid in storage order: merge-window
+// order (2x2 windows in raster order, the window's 4 tokens consecutive) when
+// merge == 2, raster order otherwise.
+__device__ __forceinline__ void decode_token(int j, int h, int w, int merge, int* ti, int* hi, int* wi) {
+  const int hw = h * w;
+  *ti = j / hw;
+  const int rem = j - *ti * hw;
+  if (merge == 2) {
+    const int win = rem >> 2, q = rem & 3, wb_n = w >> 1;
+    *hi = 2 * (win / wb_n) + (q >> 1);
+    *wi = 2 * (win % wb_n) + (q & 1);
+  } else {
+    *hi = rem / w;
+    *wi = rem - *hi * w;
+  }
+}
+
+__global__ void positions_kernel(SeqMeta m, int N, int4* pos3, int* tab_idx, int pos_gw) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= N) return;
+  const int r = find_seq(m.cu, m.n, i);
+  int j = i - m.cu[r];
+  int4 p = make_int4(0, 0, 0, 0);
+  if (m.cls) {
+    if (j == 0) { pos3[i] = p; tab_idx[i] = 0; return; }
+    j -= 1;
+  }
+  decode_token(j, m.thw[r][1], m.thw[r][2], m.merge, &p.x, &p.y, &p.z);
+  pos3[i] = p;
+  tab_idx[i] = m.cls + p.y * pos_gw + p.z;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+constexpr int LN_MAXE = 32;   // elements per lane: rows up to 64 * 32 = 2048 wide
+
+// One wave per row: mean, then the population variance of (x - mean).  The
+// reduction order is fixed, so a row's statistics depend only on that row.
+__device__ __forceinline__ void row_stats(const float* xr, int d, float eps, float* v, float* mu, float* rstd) {
+  const int lane = threadIdx.x & 63;
+  float s = 0.0f;
+#pragma unroll
+  for (int e = 0; e < LN_MAXE; ++e) {
+    const int c = lane + 64 * e;
+    v[e] = c < d ? xr[c] : 0.0f;
+    s += v[e];
+  }
+  const float mean = wave_sum(s) / (float)d;
+  float q = 0.0f;
+#pragma unroll
+  for (int e = 0; e < LN_MAXE; ++e) {
+    const int c = lane + 64 * e;
+    const float t = c < d ? v[e] - mean : 0.0f;
+    q += t * t;
+  }
+  const float var = wave_sum(q) / (float)d;
+  *mu = mean;
+  *rstd = 1.0f / sqrtf(var + eps);
+}
+
+__global__ __launch_bounds__(256) void ln_stats_kernel(const float* x, int N, int d, float eps, float2* st) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= N) return;
+  float v[LN_MAXE], mu, rstd;
+  row_stats(x + (long)row * d, d, eps, v, &mu, &rstd);
+  if ((threadIdx.x & 63) == 0) st[row] = make_float2(mu, rstd);
+}
+
+template <class W, class Y>
+__global__ __launch_bounds__(256) void ln_apply_kernel(const float* x, int N, int d, float eps, const W* g,
+                                                       const W* b, Y* y) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= N) return;
+  const int lane = threadIdx.x & 63;
+  float v[LN_MAXE], mu, rstd;
+  row_stats(x + (long)row * d, d, eps, v, &mu, &rstd);
+#pragma unroll
+  for (int e = 0; e < LN_MAXE; ++e) {
+    const int c = lane + 64 * e;
+    if (c < d) y[(long)row * d + c] = (Y)((v[e] - mu) * rstd * (float)g[c] + (float)b[c]);
+  }
+}
+
+// Rotate the pairs (k, k + hd/2) of every head of q and k in place; slot k
+// turns by pos[axis(k)] * inv_freq[k].
+template <class T>
+__global__ void rope_kernel(T* qkv, int ldqkv, int N, int heads, int hd, const int4* pos3,
+                            const float* inv_freq, const int* slot_axis) {
+  const int half = hd >> 1;
+  const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  const long total = (long)N * heads * half;
+  if (idx >= total) return;
+  const int k = (int)(idx % half);
+  const int h = (int)((idx / half) % heads);
+  const int i = (int)(idx / ((long)half * heads));
+  const int4 p = pos3[i];
+  const int ax = slot_axis[k];
+  const float pos = (float)(ax == 0 ? p.x : (ax == 1 ? p.y : p.z));
+  float sn, cs;
+  sincosf(pos * inv_freq[k], &sn, &cs);
+  const int dq = heads * hd;
+#pragma unroll
+  for (int part = 0; part < 2; ++part) {   // q block, then k block
+    T* base = qkv + (long)i * ldqkv + part * dq + h * hd;
+    const float x1 = (float)base[k], x2 = (float)base[k + half];
+    base[k] = (T)(x1 * cs - x2 * sn);
+    base[k + half] = (T)(x2 * cs + x1 * sn);
+  }
+}
+
+template <class W>
+__global__ void cls_kernel(SeqMeta m, float* x, int d, const W* cls, const W* pos0) {
+  const int r = blockIdx.x;
+  for (int c = threadIdx.x; c < d; c += blockDim.x)
+    x[(long)m.cu[r] * d + c] = (float)cls[c] + (float)pos0[c];
+}
+
+// dst[(clip, t), c*3 + k] = src[(clip, stride*t + k - 1), c], zero outside the
+// clip: the im2col of a kernel-3, padding-1 1-D convolution over time-major
+// frames, in the (channel, tap) order of a [out, C, 3] weight.
+template <class T>
+__global__ void im2col_k3_kernel(const T* src, int fin, int C, int fout, int stride, long total, T* dst) {
+  const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= total) return;
+  const int k = (int)(idx % 3);
+  const int c = (int)((idx / 3) % C);
+  const long row = idx / (3L * C);
+  const int t = (int)(row % fout);
+  const long clip = row / fout;
+  const int ts = stride * t + k - 1;
+  dst[idx] = (ts >= 0 && ts < fin) ? src[(clip * fin + ts) * C + c] : (T)0.0f;
+}
+
+template <class T>
+__global__ void pack_vision_kernel(PackArgs p, int cls, int merge, int patch, int tp, int K, long total, T* out) {
+  const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= total) return;
+  const int kk = (int)(idx % K);
+  const int row = (int)(idx / K);
+  const int r = find_seq(p.cu, p.n, row);
+  int j = row - p.cu[r];
+  if (cls) {
+    if (j == 0) { out[idx] = (T)0.0f; return; }
+    j -= 1;
+  }
+  const int H = p.tchw[r][2], W = p.tchw[r][3], C = p.tchw[r][1];
+  const int h = H / patch, w = W / patch;
+  int ti, hi, wi;
+  decode_token(j, h, w, merge, &ti, &hi, &wi);
+  const int dx = kk % patch, dy = (kk / patch) % patch;
+  const int tau = (kk / (patch * patch)) % tp, c = kk / (patch * patch * tp);
+  const long src = (((long)(ti * tp + tau) * C + c) * H + hi * patch + dy) * W + wi * patch + dx;
+  out[idx] = (T)p.src[r][src];
+}
+
+// [n_mels, n_frames] -> [n_frames, n_mels] per clip.
+template <class T>
+__global__ void pack_audio_kernel(PackArgs p, int n_mels, int n_frames, T* out) {
+  const long per = (long)n_mels * n_frames;
+  const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= per * p.n) return;
+  const int clip = (int)(idx / per);
+  const long e = idx % per;
+  const int t = (int)(e / n_mels), mel = (int)(e % n_mels);
+  out[idx] = (T)p.src[clip][(long)mel * n_frames + t];
+}
+
+inline unsigned blocks_for(long n, int bs) { return (unsigned)((n + bs - 1) / bs); }
+
+}  // namespace
+
+hipError_t launch_positions(const SeqMeta& m, int N, int4* pos3, int* tab_idx, int pos_gw, hipStream_t s) {
+  hipLaunchKernelGGL(positions_kernel, dim3(blocks_for(N, 256)), dim3(256), 0, s, m, N, pos3, tab_idx, pos_gw);
+  return hipGetLastError();
+}
+
+hipError_t launch_ln_stats(const float* x, int N, int d, float eps, float2* stats, hipStream_t s) {
+  if (d > 64 * LN_MAXE) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(ln_stats_kernel, dim3(blocks_for(N, 4)), dim3(256), 0, s, x, N, d, eps, stats);
+  return hipGetLastError();
+}
+
+hipError_t launch_ln_apply(const float* x, int N, int d, float eps, const void* g, const void* b, int w_bf16,
+                           void* y, int y_f32, hipStream_t s) {
+  if (d > 64 * LN_MAXE) return hipErrorInvalidValue;
+  const dim3 grid(blocks_for(N, 4)), blk(256);
+  if (w_bf16 && y_f32)
+    hipLaunchKernelGGL((ln_apply_kernel<bf16, float>), grid, blk, 0, s, x, N, d, eps, (const bf16*)g, (const bf16*)b, (float*)y);
+  else if (w_bf16)
+    hipLaunchKernelGGL((ln_apply_kernel<bf16, bf16>), grid, blk, 0, s, x, N, d, eps, (const bf16*)g, (const bf16*)b, (bf16*)y);
+  else if (y_f32)
+    hipLaunchKernelGGL((ln_apply_kernel<float, float>), grid, blk, 0, s, x, N, d, eps, (const float*)g, (const float*)b, (float*)y);
+  else
+    hipLaunchKernelGGL((ln_apply_kernel<float, bf16>), grid, blk, 0, s, x, N, d, eps, (const float*)g, (const float*)b, (bf16*)y);
+  return hipGetLastError();
+}
+
+hipError_t launch_rope(void* qkv, int ldqkv, int N, int heads, int hd, int is_bf16, const int4* pos3,
+                       const float* inv_freq, const int* slot_axis, hipStream_t s) {
+  const long total = (long)N * heads * (hd / 2);
+  if (is_bf16)
+    hipLaunchKernelGGL((rope_kernel<bf16>), dim3(blocks_for(total, 256)), dim3(256), 0, s, (bf16*)qkv, ldqkv, N,
+                       heads, hd, pos3, inv_freq, slot_axis);
+  else
+    hipLaunchKernelGGL((rope_kernel<float>), dim3(blocks_for(total, 256)), dim3(256), 0, s, (float*)qkv, ldqkv, N,
+                       heads, hd, pos3, inv_freq, slot_axis);
+  return hipGetLastError();
+}
+
+hipError_t launch_cls(const SeqMeta& m, float* x, int d, const void* cls, const void* pos0, int w_bf16, hipStream_t s) {
+  if (w_bf16)
+    hipLaunchKernelGGL((cls_kernel<bf16>), dim3(m.n), dim3(256), 0, s, m, x, d, (const bf16*)cls, (const bf16*)pos0);
+  else
+    hipLaunchKernelGGL((cls_kernel<float>), dim3(m.n), dim3(256), 0, s, m, x, d, (const float*)cls, (const float*)pos0);
+  return hipGetLastError();
+}
+
+hipError_t launch_im2col_k3(const void* src, int frames_in, int C, int n_clips, int stride, int is_bf16, void* dst,
+                            hipStream_t s) {
+  const int fout = (frames_in - 1) / stride + 1;
+  const long total = (long)n_clips * fout * C * 3;
+  if (is_bf16)
+    hipLaunchKernelGGL((im2col_k3_kernel<bf16>), dim3(blocks_for(total, 256)), dim3(256), 0, s, (const bf16*)src,
+                       frames_in, C, fout, stride, total, (bf16*)dst);
+  else
+    hipLaunchKernelGGL((im2col_k3_kernel<float>), dim3(blocks_for(total, 256)), dim3(256), 0, s, (const float*)src,
+                       frames_in, C, fout, stride, total, (float*)dst);
+  return hipGetLastError();
+}
+
+hipError_t launch_pack_vision(const PackArgs& p, int cls, int merge, int patch, int tp, int K, int is_bf16,
+                              void* packed, long total, hipStream_t s) {
+  if (is_bf16)
+    hipLaunchKernelGGL((pack_vision_kernel<bf16>), dim3(blocks_for(total, 256)), dim3(256), 0, s, p, cls, merge, patch,
+                       tp, K, total, (bf16*)packed);
+  else
+    hipLaunchKernelGGL((pack_vision_kernel<float>), dim3(blocks_for(total, 256)), dim3(256), 0, s, p, cls, merge,
+                       patch, tp, K, total, (float*)packed);
+  return hipGetLastError();
+}
+
+hipError_t launch_pack_audio(const PackArgs& p, int n_mels, int n_frames, int is_bf16, void* packed, hipStream_t s) {
+  const long total = (long)p.n * n_mels * n_frames;
+  if (is_bf16)
+    hipLaunchKernelGGL((pack_audio_kernel<bf16>), dim3(blocks_for(total, 256)), dim3(256), 0, s, p, n_mels, n_frames,
+                       (bf16*)packed);
+  else
+    hipLaunchKernelGGL((pack_audio_kernel<float>), dim3(blocks_for(total, 256)), dim3(256), 0, s, p, n_mels, n_frames,
+                       (float*)packed);
+  return hipGetLastError();
+}
+
+}  // namespace eas

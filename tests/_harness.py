@@ -1,0 +1,52 @@
+"""Shared helpers of the GPU parity tests: run a micro-batch through the HIP
+library (via the C ABI binding) and through the fp64 reference."""
+import numpy as np
+
+from oracle import encoder as O
+from paper_2609_31551_amd import configs as C
+
+TOL = {"bf16": 2e-2, "fp32": 1e-4}   # max|gpu - ref| / max|ref|
+
+
+def rel_err(got, ref):
+    return float(np.abs(got - ref).max() / np.abs(ref).max())
+
+
+def gpu_encode(preset, items, weights, out_dtype="fp32", enc=None, wdev=None, max_tokens=None):
+    import torch
+    from paper_2609_31551_amd import eas
+    n = len(items)
+    if enc is None:
+        tchw = [list(a.shape) if a.ndim == 4 else [1, 1] + list(a.shape) for a in items]
+        cfg0 = eas.make_config(preset, max_tokens=1 << 30, max_seqs=max(n, 1))
+        cu, _, _, _ = eas.microbatch_shape(cfg0, tchw)
+        enc = eas.Encoder(preset, max_tokens or int(cu[-1]), max_seqs=max(n, 1), out_dtype=out_dtype)
+    if wdev is None:
+        wdev = eas.upload_weights(enc.cfg, weights)
+    dev_items = [torch.from_numpy(np.ascontiguousarray(a, np.float32)).cuda() for a in items]
+    packed, cu, grid = enc.pack_microbatch(dev_items)
+    grid_arg = None if preset["kind"] == C.KIND_WHISPER else grid
+    out, cu_out = enc.encode_microbatch(packed, cu, grid_arg, wdev)
+    torch.cuda.synchronize()
+    return dict(out=out.float().cpu().numpy(), cu_out=cu_out, cu=cu, grid=grid,
+                packed=packed.float().cpu().numpy(), enc=enc, wdev=wdev)
+
+
+def oracle_encode(preset, items, weights):
+    packed, cu, grid = O.pack(preset, items)
+    out, cu_out = O.encode(preset, weights, packed, cu, grid)
+    return dict(out=out, cu_out=cu_out, cu=cu, grid=grid, packed=packed)
+
+
+def check_parity(preset, got, ref, tol=None):
+    """Whole-batch and per-request error bound; returns the worst error."""
+    tol = TOL[preset["dtype"]] if tol is None else tol
+    np.testing.assert_array_equal(got["cu_out"], ref["cu_out"])
+    worst = rel_err(got["out"], ref["out"])
+    assert worst <= tol, "batch error %.3g > %.3g" % (worst, tol)
+    cu = ref["cu_out"]
+    for r in range(len(cu) - 1):
+        e = rel_err(got["out"][cu[r]:cu[r + 1]], ref["out"][cu[r]:cu[r + 1]])
+        assert e <= tol, "request %d error %.3g > %.3g" % (r, e, tol)
+        worst = max(worst, e)
+    return worst

@@ -1,0 +1,91 @@
+"""Host-side checks of the C ABI: the library loads, exports every symbol the
+header declares, lays weights out in the canonical order, and rejects bad
+micro-batches before any device work.  No GPU needed (no HIP compute call)."""
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2609_31551_amd import configs as C
+from paper_2609_31551_amd import eas
+from paper_2609_31551_amd import synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "eas_encoder.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:eas_status|void|const char\*)\s+(eas_\w+)\s*\(", text, re.M)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert len(names) >= 10
+    for n in names:
+        assert hasattr(eas.LIB, n), n
+    assert sorted(eas.EXPORTS) == names
+
+
+@pytest.mark.parametrize("preset", list(C.PRESETS.values()), ids=list(C.PRESETS))
+def test_weight_layout_matches_generator_tensor_list(preset):
+    cfg = eas.make_config(C.with_layers(preset, 2), max_tokens=1024)
+    layout, total = eas.weights_layout(cfg)
+    specs = synth.weight_specs(C.with_layers(preset, 2))
+    assert [n for n, _, _ in layout] == [n for n, _, _ in specs]
+    assert [tuple(s) for _, _, s in layout] == [tuple(s) for _, s, _ in specs]
+    el = 2 if preset["dtype"] == "bf16" else 4
+    offs = [o for _, o, _ in layout]
+    assert offs[0] == 0 and all(o % 256 == 0 for o in offs)
+    for (n, o, s), o2 in zip(layout, offs[1:] + [total]):
+        assert o + int(np.prod(s)) * el <= o2
+
+
+def test_microbatch_shape_counts_tokens_and_cls():
+    cfg = eas.make_config(C.CLIP_L336, max_tokens=4096, max_seqs=8)
+    cu, grid, elems, rows = eas.microbatch_shape(cfg, [[1, 3, 336, 336]] * 3)
+    assert cu.tolist() == [0, 577, 1154, 1731]
+    assert grid.tolist() == [[1, 24, 24]] * 3
+    assert elems == 1731 * 588 and rows == 1731
+    cfg = eas.make_config(C.QWEN_IMAGE, max_tokens=100000, max_seqs=8)
+    cu, grid, elems, rows = eas.microbatch_shape(cfg, [[2, 3, 224, 308], [2, 3, 1344, 672]])
+    assert cu.tolist() == [0, 16 * 22, 16 * 22 + 96 * 48]
+    assert grid.tolist() == [[1, 16, 22], [1, 96, 48]]
+    assert rows == cu[-1] // 4 and elems == cu[-1] * 1176
+    cfg = eas.make_config(C.WHISPER_L, max_tokens=10000, max_seqs=8)
+    cu, _, elems, rows = eas.microbatch_shape(cfg, [[1, 1, 128, 3000]] * 2)
+    assert cu.tolist() == [0, 1500, 3000] and elems == 2 * 128 * 3000 and rows == 3000
+
+
+def test_validate_accepts_good_and_rejects_bad_batches():
+    cfg = eas.make_config(C.QWEN_IMAGE, max_tokens=2000, max_seqs=4)
+    good_grid = [[1, 16, 22], [1, 8, 8]]
+    assert eas.validate_microbatch(cfg, [0, 352, 416], good_grid) == eas.EAS_OK
+    assert eas.validate_microbatch(cfg, [1, 352, 416], good_grid) == eas.EAS_ERR_SHAPE          # cu[0] != 0
+    assert eas.validate_microbatch(cfg, [0, 352, 352], good_grid) == eas.EAS_ERR_SHAPE          # not increasing
+    assert eas.validate_microbatch(cfg, [0, 350, 414], good_grid) == eas.EAS_ERR_SHAPE          # grid mismatch
+    assert eas.validate_microbatch(cfg, [0, 15 * 22, 15 * 22 + 64], [[1, 15, 22], [1, 8, 8]]) == eas.EAS_ERR_SHAPE  # odd h
+    assert eas.validate_microbatch(cfg, [0, 2112], [[1, 48, 44]]) == eas.EAS_ERR_CAPACITY     # > max_tokens
+    assert eas.validate_microbatch(cfg, [0] + [64] * 5, [[1, 8, 8]] * 5, 5) == eas.EAS_ERR_CAPACITY  # > max_seqs
+    assert eas.validate_microbatch(cfg, [0, 352], None) == eas.EAS_ERR_INVALID_ARG            # grid required
+    cfgc = eas.make_config(C.CLIP_L336, max_tokens=4096, max_seqs=4)
+    assert eas.validate_microbatch(cfgc, [0, 577], [[1, 24, 24]]) == eas.EAS_OK
+    assert eas.validate_microbatch(cfgc, [0, 576], [[1, 24, 24]]) == eas.EAS_ERR_SHAPE        # CLS token missing
+    assert eas.validate_microbatch(cfgc, [0, 626], [[1, 25, 25]]) == eas.EAS_ERR_SHAPE        # beyond the pos table
+    cfgw = eas.make_config(C.WHISPER_L, max_tokens=4096, max_seqs=4)
+    assert eas.validate_microbatch(cfgw, [0, 1500, 3000], None) == eas.EAS_OK
+    assert eas.validate_microbatch(cfgw, [0, 1500, 2999], None) == eas.EAS_ERR_SHAPE
+
+
+def test_config_errors_are_reported_without_hip():
+    bad = dict(C.CLIP_L336, heads=15)
+    cfg = eas.make_config(bad, max_tokens=10)
+    assert eas.validate_microbatch(cfg, [0, 577], [[1, 24, 24]]) == eas.EAS_ERR_INVALID_ARG
+    odd = dict(C.QWEN_IMAGE, head_dim=40, heads=32, rope_sections=(0, 10, 10))
+    cfg = eas.make_config(odd, max_tokens=10)
+    assert eas.validate_microbatch(cfg, [0, 4], [[1, 2, 2]]) == eas.EAS_ERR_UNSUPPORTED
+    with pytest.raises(eas.EasError):
+        eas.weights_layout(eas.make_config(dict(C.QWEN_IMAGE, rope_sections=(0, 20, 19)), max_tokens=10))
+    with pytest.raises(eas.EasError):
+        eas.microbatch_shape(eas.make_config(C.QWEN_IMAGE, max_tokens=10 ** 6), [[2, 3, 230, 308]])
