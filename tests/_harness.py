@@ -49,4 +49,5 @@ def check_parity(preset, got, ref, tol=None):
         e = rel_err(got["out"][cu[r]:cu[r + 1]], ref["out"][cu[r]:cu[r + 1]])
         assert e <= tol, "request %d error %.3g > %.3g" % (r, e, tol)
         worst = max(worst, e)
+    print("[parity] %s: worst relative error %.3g (tol %.0e)" % (preset["name"], worst, tol), flush=True)
     return worst
