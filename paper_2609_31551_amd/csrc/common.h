@@ -75,6 +75,7 @@ struct GemmArgs {
 
 // ---- launchers (each returns hipGetLastError() of its launch) --------------
 hipError_t launch_gemm_bf16(const GemmArgs& a, hipStream_t s, const char** kname);
+hipError_t launch_gemm_bf16_staged(const GemmArgs& a, hipStream_t s, const char** kname);
 hipError_t launch_gemm_f32(const GemmArgs& a, hipStream_t s, const char** kname);
 
 struct AttnArgs {

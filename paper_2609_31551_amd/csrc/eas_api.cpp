@@ -226,6 +226,7 @@ struct eas_encoder {
   void* qkv = nullptr;       // [max_tokens, 3d]
   void* ao = nullptr;        // attention output [max_tokens, d]
   void* hbuf = nullptr;      // MLP hidden [max_tokens, max(f, 4d, 3d)]
+  void* xn = nullptr;        // LayerNorm output [max_tokens, d] (bf16 models)
   int4* pos3 = nullptr;      // (t, h, w) per token
   int* tab_idx = nullptr;    // learned-position row per token
   float* sinus = nullptr;    // [n_frames/2, d] (WHISPER)
@@ -296,6 +297,32 @@ eas_status gemm(eas_encoder* e, const GemmArgs& g, hipStream_t s) {
   return run(e, s, flops, bytes, [&](const char** kn) {
     return bf ? launch_gemm_bf16(g, s, kn) : launch_gemm_f32(g, s, kn);
   });
+}
+
+// LN(x) * W^T: fp32 models fuse the LayerNorm into the GEMM's A loader; bf16
+// models write the normalised rows once as bf16 and run the plain GEMM.
+// x is [M * group, dim] fp32 viewed as M rows of group * dim.
+eas_status ln_gemm(eas_encoder* e, GemmArgs g, float eps, int group, hipStream_t s) {
+  const int dim = g.ln_dim, rows = g.M * group;
+  const float* x = static_cast<const float*>(g.A);
+  if (e->cfg.dtype != EAS_BF16) {
+    eas_status rc = run(e, s, 0.0, (double)rows * (dim * 4 + 8), [&](const char** kn) {
+      *kn = "ln_stats";
+      return launch_ln_stats(x, rows, dim, eps, e->stats, s);
+    });
+    if (rc != EAS_OK) return rc;
+    g.stats = e->stats;
+    g.ln_group = group;
+    return gemm(e, g, s);
+  }
+  eas_status rc = run(e, s, 0.0, (double)rows * dim * 6, [&](const char** kn) {
+    *kn = "ln_apply_bf16";
+    return launch_ln_apply(x, rows, dim, eps, g.ln_g, g.ln_b, 1, e->xn, 0, s);
+  });
+  if (rc != EAS_OK) return rc;
+  g.A = e->xn;   // same [M, group * dim] view, now bf16
+  g.ln_g = g.ln_b = nullptr;
+  return gemm(e, g, s);
 }
 
 const char* wptr(const void* weights, const eas_encoder* e, const std::string& name) {
@@ -400,9 +427,9 @@ eas_status eas_encoder_create(const eas_config* cfg, eas_encoder** out) {
   }
   auto al = [](int64_t b) { return (b + 255) / 256 * 256; };
   const int64_t half = d / c.heads / 2;
-  int64_t sz[9] = {al(N * d * 4), al(N * 8), al(qkv_rows * 3 * d * el), al(ao_rows * d * el), al(N * hw * el),
-                   al(N * 16), al(N * 4), al(c.kind == EAS_KIND_WHISPER ? (int64_t)c.n_frames / 2 * d * 4 : 256),
-                   al(half * 8 + 256)};
+  int64_t sz[10] = {al(N * d * 4), al(N * 8), al(qkv_rows * 3 * d * el), al(ao_rows * d * el), al(N * hw * el),
+                    al(N * 16), al(N * 4), al(c.kind == EAS_KIND_WHISPER ? (int64_t)c.n_frames / 2 * d * 4 : 256),
+                    al(half * 8 + 256), al(N * d * el)};
   int64_t total = 0;
   for (int64_t v : sz) total += v;
   if (hipMalloc(&e->ws, total) != hipSuccess) {
@@ -420,6 +447,8 @@ eas_status eas_encoder_create(const eas_config* cfg, eas_encoder** out) {
   e->sinus = (float*)p; p += sz[7];
   e->inv_freq = (float*)p;
   e->slot_axis = (int*)(p + al(half * 4));
+  p += sz[8];
+  e->xn = p;
   hipError_t herr = hipSuccess;
   if (c.kind == EAS_KIND_WHISPER) {   // Whisper-style sinusoid table, computed in double
     const int64_t F = c.n_frames / 2, hc = d / 2;
@@ -664,17 +693,12 @@ eas_status eas_encode_microbatch(eas_encoder* enc, const void* packed_in, const 
   const int mid_f32 = bf ? 0 : 1;   // qkv / attention / MLP activations: model dtype
   for (int l = 0; l < c.layers; ++l) {
     const std::string p = "layers." + std::to_string(l) + ".";
-    EAS_TRY(run(enc, s, 0.0, (double)N * (d * 4 + 8), [&](const char** kn) {
-      *kn = "ln_stats";
-      return launch_ln_stats(enc->x, N, d, c.ln_eps, enc->stats, s);
-    }));
     GemmArgs gq = gemm_args(N, d3, d, enc->x, d, W(p + "qkv.w"), d, enc->qkv, d3, mid_f32);
-    gq.stats = enc->stats;
     gq.ln_g = W(p + "ln1.g");
     gq.ln_b = W(p + "ln1.b");
     gq.ln_dim = d;
     gq.bias = W(p + "qkv.b");
-    EAS_TRY(gemm(enc, gq, s));
+    EAS_TRY(ln_gemm(enc, gq, c.ln_eps, 1, s));
     if (c.kind == EAS_KIND_VIT_ROPE)
       EAS_TRY(run(enc, s, 0.0, (double)N * 2 * d * el * 2 + (double)N * 16, [&](const char** kn) {
         *kn = "rope";
@@ -696,18 +720,13 @@ eas_status eas_encode_microbatch(eas_encoder* enc, const void* packed_in, const 
     go.resid = enc->x;
     go.ldr = d;
     EAS_TRY(gemm(enc, go, s));
-    EAS_TRY(run(enc, s, 0.0, (double)N * (d * 4 + 8), [&](const char** kn) {
-      *kn = "ln_stats";
-      return launch_ln_stats(enc->x, N, d, c.ln_eps, enc->stats, s);
-    }));
     GemmArgs g1 = gemm_args(N, f, d, enc->x, d, W(p + "fc1.w"), d, enc->hbuf, f, mid_f32);
-    g1.stats = enc->stats;
     g1.ln_g = W(p + "ln2.g");
     g1.ln_b = W(p + "ln2.b");
     g1.ln_dim = d;
     g1.bias = W(p + "fc1.b");
     g1.act = act;
-    EAS_TRY(gemm(enc, g1, s));
+    EAS_TRY(ln_gemm(enc, g1, c.ln_eps, 1, s));
     // the CLS model's output is the final residual stream: the last FC2 writes it directly
     const bool direct = c.kind == EAS_KIND_VIT_CLS_ABS && l == c.layers - 1;
     GemmArgs g2 = gemm_args(N, d, f, enc->hbuf, f, W(p + "fc2.w"), f, direct ? out_embeddings : (void*)enc->x, d,
@@ -720,20 +739,14 @@ eas_status eas_encode_microbatch(eas_encoder* enc, const void* packed_in, const 
 
   // ---- connector ----
   if (c.merge == 2) {
-    EAS_TRY(run(enc, s, 0.0, (double)N * (d * 4 + 8), [&](const char** kn) {
-      *kn = "ln_stats";
-      return launch_ln_stats(enc->x, N, d, c.merger_ln_eps, enc->stats, s);
-    }));
     const int G = N / 4, d4 = 4 * d;
     GemmArgs m1 = gemm_args(G, d4, d4, enc->x, d4, W("m1.w"), d4, enc->hbuf, d4, mid_f32);
-    m1.stats = enc->stats;
     m1.ln_g = W("ln_q.g");
     m1.ln_b = W("ln_q.b");
     m1.ln_dim = d;
-    m1.ln_group = 4;
     m1.bias = W("m1.b");
     m1.act = ACT_GELU;
-    EAS_TRY(gemm(enc, m1, s));
+    EAS_TRY(ln_gemm(enc, m1, c.merger_ln_eps, 4, s));
     GemmArgs m2 = gemm_args(G, c.out_dim, d4, enc->hbuf, d4, W("m2.w"), d4, out_embeddings, c.out_dim, out_f32);
     m2.bias = W("m2.b");
     EAS_TRY(gemm(enc, m2, s));

@@ -1,249 +1,314 @@
-// bf16 MFMA GEMM for the encoder's dense projections (patch embedding, QKV,
-// attention output, MLP, merger).  C[m, n] = sum_k A[m, k] * B[n, k]: both
-// operands are K-contiguous ("NT"), the natural layout of activations
+// bf16 MFMA GEMM for the encoder's dense projections (QKV, attention output,
+// MLP, merger, audio front end).  C[m, n] = sum_k A[m, k] * B[n, k]: both
+// operands K-contiguous ("NT"), the natural layout of activations
 // [tokens, in] and of Linear weights [out, in].
 //
-// Design (gfx950):
-//  * v_mfma_f32_32x32x16_bf16: each lane feeds 8 consecutive k of one row of
-//    A and of B straight from a 16-byte LDS read; fp32 accumulators.
-//  * Workgroup tile BM x BN, k-step 64; waves in a (BM/WM) x (BN/WN) grid,
-//    each a WM x WN sub-tile of (WM/32) x (WN/32) MFMA blocks: 256 x 256 with
-//    4 waves of 128 x 128 (accumulators in AGPRs), or 128 x 128 with 4 waves
-//    of 64 x 64.
-//  * Two LDS stages: the global loads of step k+1 are issued before the MFMAs
-//    of step k and written to the other stage after them, so one barrier per
-//    k-step suffices.  LDS rows are padded by 16 bytes so the 32 rows one
-//    16-byte read touches land on distinct banks.
-//  * LayerNorm prologue: with `stats`, A is the fp32 residual stream and the
-//    loader applies (x - mean) * rstd * g + b before rounding to bf16, so no
-//    normalised copy of the activations ever goes to HBM.
-//  * Fused epilogue: bias, GELU / QuickGELU, position-table add and fp32
-//    residual add, then one store (fp32 or bf16).  Accumulators go through
-//    LDS one 32-row slab per wave, so the residual reads and the output
-//    stores walk rows with the 64 lanes on consecutive columns.
-//  * Each output element accumulates k in the same order (16-wide MFMA
-//    steps, ascending) whatever the tile shape or M, so a request's result
-//    does not depend on what else is in the micro-batch.
+// Design (gfx950, one workgroup per BM x BN output tile):
+//  * Operands reach LDS by direct DMA: global_load_lds_dwordx4 moves 16 bytes
+//    per lane from HBM/L2 into LDS without passing through VGPRs.  One wave
+//    instruction fills 1 KB = 16 rows x 64 bytes (a 32-wide k-slice of bf16).
+//    The lane -> (row, 16-byte chunk) assignment applies an XOR swizzle
+//    (chunk ^ ((row >> 1) & 3)) so that the MFMA operand reads, 32 rows at a
+//    time at one k offset, spread over all LDS banks.
+//  * k-step 32, 4 LDS stages: tile k+3 is in flight while tile k is
+//    consumed.  The DMA is issued from inline assembly so the compiler does
+//    not serialise it against the LDS reads; completion is tracked with
+//    explicit s_waitcnt vmcnt and one workgroup barrier per k-step.
+//  * v_mfma_f32_32x32x16_bf16, each wave a (BM/WGM) x (BN/WGN) sub-tile of
+//    32 x 32 blocks; operand fragments for the second 16-wide half of a
+//    k-step are read while the first half's MFMAs run, and the barrier sits
+//    between the halves so its wait overlaps queued MFMAs.
+//  * Tiles are handed out XCD-aware: workgroups are dispatched round-robin
+//    over the 8 XCDs, so block b is remapped to give every XCD a contiguous
+//    run of output tiles that share A row panels in that XCD's L2.
+//  * Fused epilogue through LDS: each wave stages 32 rows of its fp32
+//    accumulators, then every lane owns 8 consecutive columns of a row and
+//    applies bias, GELU / QuickGELU, a position-table row and the fp32
+//    residual before one 16-byte (bf16) or 2 x 16-byte (fp32) store.
+//  * Every output element accumulates k in the same order (32-wide k-steps,
+//    two 16-wide MFMA halves, ascending) whatever the tile shape or M, so a
+//    request's result does not depend on what else is in the micro-batch.
 #include "common.h"
 
 namespace eas {
 namespace {
 
-constexpr int BK = 64;
-constexpr int LDK = BK + 8;   // padded LDS row (bf16 elements)
+constexpr int BK = 32, ST = 4;
 
-template <int BM, int BN, int WM, int WN>
-struct Tile {
-  static constexpr int WAVES_N = BN / WN;
-  static constexpr int NT = 64 * (BM / WM) * (BN / WN);
+// M0 carries the LDS base of each DMA; nothing else in these kernels uses M0
+// (checked in the generated code), so setting it here cannot disturb the
+// compiler's own code even though it treats M0 as reserved.
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void dma16(unsigned lds_addr, unsigned voff, const void* gbase) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2\n"
+               :: "s"(lds_addr), "v"(voff), "s"(gbase) : "memory", "m0");
+}
+template <int N> __device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" :: "n"(N) : "memory");
+}
+__device__ __forceinline__ void wait_lds() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
+template <int BM, int BN, int WGM, int WGN>
+struct Cfg {
+  static constexpr int NW = WGM * WGN, NT = 64 * NW;
+  static constexpr int WM = BM / WGM, WN = BN / WGN;
   static constexpr int FM = WM / 32, FN = WN / 32;
-  static constexpr int CPR = BK / 8;            // 8-element chunks per tile row
-  static constexpr int A_CH = BM * CPR / NT;    // A chunks per thread per stage
-  static constexpr int B_CH = BN * CPR / NT;
-  static constexpr int STAGE = (BM + BN) * LDK; // bf16 elements per LDS stage
+  static constexpr int TA = BM * BK * 2, TB = BN * BK * 2, STAGE = TA + TB;
+  static constexpr int DA = BM / 16 / NW, DB = BN / 16 / NW;   // DMA instructions per wave per stage
+  static constexpr int DPS = DA + DB;
+  static constexpr int SLD = WN + 4;                            // epilogue slab row (floats)
+  static constexpr int LDS = ST * STAGE > NW * 32 * SLD * 4 ? ST * STAGE : NW * 32 * SLD * 4;
+  static_assert(BM % (16 * NW) == 0 && BN % (16 * NW) == 0, "DMA split");
+  static_assert(3 * DPS < 64, "vmcnt range");
 };
 
-__device__ __forceinline__ uint4 load16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
-
-// Bounds-checked 8-element load of row `r`, columns k..k+7 (zero outside).
-__device__ __forceinline__ uint4 load8_checked(const bf16* base, int ld, int r, int rows, int k, int K) {
-  union { uint4 u; bf16 h[8]; } v;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) v.h[e] = (r < rows && k + e < K) ? base[(long)r * ld + k + e] : (bf16)0.0f;
-  return v.u;
+// XCD-aware block -> tile index (bijective on [0, nb)).
+__device__ __forceinline__ int xcd_tile(int b, int nb) {
+  const int per = (nb + 7) / 8, x = b % 8, s = b / 8;
+  const int full = nb % 8 == 0 ? 8 : nb % 8;   // XCDs that receive `per` blocks
+  return (x < full ? x * per : full * per + (x - full) * (per - 1)) + s;
 }
 
-template <int BM, int BN, int WM, int WN, bool LN, bool GENERIC>
-__global__ __launch_bounds__(64 * (BM / WM) * (BN / WN)) void gemm_bf16_kernel(GemmArgs a) {
-  using T = Tile<BM, BN, WM, WN>;
-  __shared__ __attribute__((aligned(16))) bf16 smem[2 * T::STAGE];
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / T::WAVES_N, wn = wave % T::WAVES_N;
+template <int BM, int BN, int WGM, int WGN>
+__global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_tile_kernel(GemmArgs a) {
+  using C = Cfg<BM, BN, WGM, WGN>;
+  extern __shared__ __attribute__((aligned(1024))) char smem[];
+  const unsigned lds0 = (unsigned)(size_t)((__attribute__((address_space(3))) char*)smem);
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / WGN, wn = wave % WGN;
   const int tiles_n = (a.N + BN - 1) / BN;
-  const int m0 = (blockIdx.x / tiles_n) * BM, n0 = (blockIdx.x % tiles_n) * BN;
-  const int KT = (a.K + BK - 1) / BK;
+  const int bid = xcd_tile(blockIdx.x, gridDim.x);
+  const int m0 = (bid / tiles_n) * BM, n0 = (bid % tiles_n) * BN;
+  const int KT = a.K / BK;
+  const bf16* A = static_cast<const bf16*>(a.A);
+  const bf16* B = static_cast<const bf16*>(a.B);
 
-  const bf16* Ab = static_cast<const bf16*>(a.A);
-  const float* Af = static_cast<const float*>(a.A);
-  const bf16* Bb = static_cast<const bf16*>(a.B);
-
-  // staging registers for one stage
-  uint4 ra[LN ? 1 : T::A_CH];
-  float4 rf[LN ? 2 * T::A_CH : 1];
-  float2 rst[LN ? T::A_CH : 1];
-  uint4 rg, rb;
-  uint4 rbw[T::B_CH];
-
-  auto load_stage = [&](int kt) {
-    const int k0 = kt * BK;
+  // DMA sources: instruction j of this wave fills tile rows (wave*D + j)*16 .. +16;
+  // lane i -> row +i/4, physical chunk i%4 holding logical chunk (i%4) ^ ((row>>1)&3).
+  // Rows past M or N re-read the last row; their results are never stored.
+  unsigned a_off[C::DA], b_off[C::DB];
+  {
+    const int c = (lane & 3) ^ ((lane >> 3) & 3);
 #pragma unroll
-    for (int i = 0; i < T::A_CH; ++i) {
-      const int c = tid + i * T::NT, row = c / T::CPR, kc = (c % T::CPR) * 8;
-      const int gm = m0 + row, gk = k0 + kc;
-      if constexpr (LN) {
-        const int r = gm < a.M ? gm : a.M - 1;
-        const float* p = Af + (long)r * a.lda + gk;
-        rf[2 * i] = *reinterpret_cast<const float4*>(p);
-        rf[2 * i + 1] = *reinterpret_cast<const float4*>(p + 4);
-        rst[i] = a.stats[(long)r * a.ln_group + gk / a.ln_dim];
-        if (i == 0) {
-          const int kk = gk % a.ln_dim;
-          rg = load16(static_cast<const bf16*>(a.ln_g) + kk);
-          rb = load16(static_cast<const bf16*>(a.ln_b) + kk);
-        }
-      } else if constexpr (GENERIC) {
-        ra[i] = load8_checked(Ab, a.lda, gm, a.M, gk, a.K);
-      } else {
-        const int r = gm < a.M ? gm : a.M - 1;
-        ra[i] = load16(Ab + (long)r * a.lda + gk);
-      }
+    for (int j = 0; j < C::DA; ++j) {
+      const int gm = min(m0 + (wave * C::DA + j) * 16 + (lane >> 2), a.M - 1);
+      a_off[j] = (unsigned)(((long)gm * a.lda + c * 8) * 2);
     }
 #pragma unroll
-    for (int i = 0; i < T::B_CH; ++i) {
-      const int c = tid + i * T::NT, row = c / T::CPR, kc = (c % T::CPR) * 8;
-      const int gn = n0 + row, gk = k0 + kc;
-      if constexpr (GENERIC) {
-        rbw[i] = load8_checked(Bb, a.ldb, gn, a.N, gk, a.K);
-      } else {
-        const int r = gn < a.N ? gn : a.N - 1;
-        rbw[i] = load16(Bb + (long)r * a.ldb + gk);
-      }
+    for (int j = 0; j < C::DB; ++j) {
+      const int gn = min(n0 + (wave * C::DB + j) * 16 + (lane >> 2), a.N - 1);
+      b_off[j] = (unsigned)(((long)gn * a.ldb + c * 8) * 2);
     }
+  }
+  auto issue = [&](int kt, int st) {
+    const unsigned base = lds0 + st * C::STAGE;
+    const bf16* ga = A + kt * BK;
+    const bf16* gb = B + kt * BK;
+#pragma unroll
+    for (int j = 0; j < C::DA; ++j) dma16(base + (wave * C::DA + j) * 1024, a_off[j], ga);
+#pragma unroll
+    for (int j = 0; j < C::DB; ++j) dma16(base + C::TA + (wave * C::DB + j) * 1024, b_off[j], gb);
   };
 
-  auto store_stage = [&](int buf) {
-    bf16* As = smem + buf * T::STAGE;
-    bf16* Bs = As + BM * LDK;
-#pragma unroll
-    for (int i = 0; i < T::A_CH; ++i) {
-      const int c = tid + i * T::NT, row = c / T::CPR, kc = (c % T::CPR) * 8;
-      if constexpr (LN) {
-        union { uint4 u; bf16 h[8]; } g, b, o;
-        g.u = rg; b.u = rb;
-        const float x[8] = {rf[2 * i].x, rf[2 * i].y, rf[2 * i].z, rf[2 * i].w,
-                            rf[2 * i + 1].x, rf[2 * i + 1].y, rf[2 * i + 1].z, rf[2 * i + 1].w};
-#pragma unroll
-        for (int e = 0; e < 8; ++e)
-          o.h[e] = (bf16)((x[e] - rst[i].x) * rst[i].y * (float)g.h[e] + (float)b.h[e]);
-        *reinterpret_cast<uint4*>(As + row * LDK + kc) = o.u;
-      } else {
-        *reinterpret_cast<uint4*>(As + row * LDK + kc) = ra[i];
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < T::B_CH; ++i) {
-      const int c = tid + i * T::NT, row = c / T::CPR, kc = (c % T::CPR) * 8;
-      *reinterpret_cast<uint4*>(Bs + row * LDK + kc) = rbw[i];
-    }
-  };
+  // operand fragment addresses: row wm*WM + i*32 + lane%32, logical chunk 2*half + lane/32
+  const int lrow = lane & 31, g = lane >> 5, sw = (lrow >> 1) & 3;
+  const int a_row = (wm * C::WM + lrow) * 64, b_row = (wn * C::WN + lrow) * 64;
+  const int cofs0 = ((0 + g) ^ sw) << 4, cofs1 = ((2 + g) ^ sw) << 4;
 
-  f32x16 acc[T::FM][T::FN];
+  f32x16 acc[C::FM][C::FN];
 #pragma unroll
-  for (int i = 0; i < T::FM; ++i)
+  for (int i = 0; i < C::FM; ++i)
 #pragma unroll
-    for (int j = 0; j < T::FN; ++j)
+    for (int j = 0; j < C::FN; ++j)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
 
-  load_stage(0);
-  store_stage(0);
-  __syncthreads();
+  bf16x8 fa0[C::FM], fb0[C::FN], fa1[C::FM], fb1[C::FN];
+  auto load_frags = [&](int st, int cofs, bf16x8* fa, bf16x8* fb) {
+    const char* As = smem + st * C::STAGE;
+    const char* Bs = As + C::TA;
+#pragma unroll
+    for (int i = 0; i < C::FM; ++i) fa[i] = *reinterpret_cast<const bf16x8*>(As + a_row + i * 32 * 64 + cofs);
+#pragma unroll
+    for (int j = 0; j < C::FN; ++j) fb[j] = *reinterpret_cast<const bf16x8*>(Bs + b_row + j * 32 * 64 + cofs);
+  };
+  auto mma = [&](const bf16x8* fa, const bf16x8* fb) {
+#pragma unroll
+    for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+      for (int j = 0; j < C::FN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+  };
 
-  const int lrow = lane & 31, lk = (lane >> 5) * 8;
+  // prologue: tiles 0 .. ST-1 in flight; wait for tile 0
+#pragma unroll
+  for (int s = 0; s < ST; ++s)
+    if (s < KT) issue(s, s);
+  {
+    const int later = KT - 1 < ST - 1 ? KT - 1 : ST - 1;   // tiles issued after tile 0
+    if (later >= 3) wait_vm<3 * C::DPS>();
+    else if (later == 2) wait_vm<2 * C::DPS>();
+    else if (later == 1) wait_vm<C::DPS>();
+    else wait_vm<0>();
+  }
+  __syncthreads();
+  load_frags(0, cofs0, fa0, fb0);
+
   for (int kt = 0; kt < KT; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < KT) load_stage(kt + 1);
-    const bf16* As = smem + cur * T::STAGE;
-    const bf16* Bs = As + BM * LDK;
-#pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      bf16x8 af[T::FM], bfg[T::FN];
-#pragma unroll
-      for (int i = 0; i < T::FM; ++i)
-        af[i] = *reinterpret_cast<const bf16x8*>(As + (wm * WM + i * 32 + lrow) * LDK + ks * 16 + lk);
-#pragma unroll
-      for (int j = 0; j < T::FN; ++j)
-        bfg[j] = *reinterpret_cast<const bf16x8*>(Bs + (wn * WN + j * 32 + lrow) * LDK + ks * 16 + lk);
-#pragma unroll
-      for (int i = 0; i < T::FM; ++i)
-#pragma unroll
-        for (int j = 0; j < T::FN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfg[j], acc[i][j], 0, 0, 0);
+    const int st = kt % ST;
+    load_frags(st, cofs1, fa1, fb1);
+    mma(fa0, fb0);
+    if (kt + 1 < KT) {
+      // this wave's reads of stage st are done once lgkmcnt drains; tile kt+1 has
+      // landed once at most the tiles issued after it are outstanding; after the
+      // barrier every wave is past stage st, which is refilled with tile kt+ST
+      wait_lds();
+      const int later = KT - 2 - kt;
+      if (later >= 2) wait_vm<2 * C::DPS>();
+      else if (later == 1) wait_vm<C::DPS>();
+      else wait_vm<0>();
+      __builtin_amdgcn_s_barrier();
+      if (kt + ST < KT) issue(kt + ST, st);
+      load_frags((kt + 1) % ST, cofs0, fa0, fb0);
     }
-    if (kt + 1 < KT) store_stage(cur ^ 1);
-    __syncthreads();
+    mma(fa1, fb1);
   }
 
-  // ---- fused epilogue, staged through LDS one 32-row slab per wave ----
-  constexpr int SLD = WN + 4;   // padded slab row (floats)
-  float* slab = reinterpret_cast<float*>(smem) + wave * 32 * SLD;
-  const bf16* bias = static_cast<const bf16*>(a.bias);
+  // ---- fused epilogue: per wave, 32-row slabs of its WM x WN sub-tile through LDS ----
+  wait_lds();
+  __builtin_amdgcn_s_barrier();
+  float* slab = reinterpret_cast<float*>(smem) + wave * 32 * C::SLD;
+  constexpr int LPR = C::WN / 8;   // lanes per row, 8 columns each
+  constexpr int RPP = 64 / LPR;    // rows per pass
+  const int prow = lane / LPR, pc = (lane % LPR) * 8;
+  const int n = n0 + wn * C::WN + pc;
+  const bool nok = n < a.N;        // N % 8 == 0: a lane's 8 columns are all in or all out
+  float bv[8];
+  {
+    const bf16* bias = static_cast<const bf16*>(a.bias);
 #pragma unroll
-  for (int i = 0; i < T::FM; ++i) {
-    __syncthreads();
+    for (int e = 0; e < 8; ++e) bv[e] = (bias && nok) ? (float)bias[n + e] : 0.0f;
+  }
+  const int act = a.act;
 #pragma unroll
-    for (int j = 0; j < T::FN; ++j)
+  for (int i = 0; i < C::FM; ++i) {
+#pragma unroll
+    for (int j = 0; j < C::FN; ++j)
 #pragma unroll
       for (int e = 0; e < 16; ++e)
-        slab[((e >> 2) * 8 + (lane >> 5) * 4 + (e & 3)) * SLD + j * 32 + lrow] = acc[i][j][e];
-    __syncthreads();
-    const int mrow0 = m0 + wm * WM + i * 32;
-#pragma unroll 1
-    for (int r = 0; r < 32; ++r) {
-      const int m = mrow0 + r;
-      if (m >= a.M) break;
-      const int pr = a.pos ? (a.pos_idx ? a.pos_idx[m] : m % a.pos_period) : 0;
+        slab[((e >> 2) * 8 + g * 4 + (e & 3)) * C::SLD + j * 32 + lrow] = acc[i][j][e];
+    wait_lds();
+    __builtin_amdgcn_wave_barrier();
+    const int mrow0 = m0 + wm * C::WM + i * 32;
+#pragma unroll 2
+    for (int p = 0; p < 32 / RPP; ++p) {
+      const int r = p * RPP + prow, m = mrow0 + r;
+      if (m < a.M && nok) {
+        const float4 s0 = *reinterpret_cast<const float4*>(slab + r * C::SLD + pc);
+        const float4 s1 = *reinterpret_cast<const float4*>(slab + r * C::SLD + pc + 4);
+        float v[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
 #pragma unroll
-      for (int c = lane; c < WN; c += 64) {
-        const int n = n0 + wn * WN + c;
-        if (n >= a.N) continue;
-        float v = apply_act(a.act, slab[r * SLD + c] + (bias ? (float)bias[n] : 0.0f));
-        if (a.pos) {
-          const long pi = (long)pr * a.ld_pos + n;
-          v += a.pos_f32 ? static_cast<const float*>(a.pos)[pi] : (float)static_cast<const bf16*>(a.pos)[pi];
+        for (int e = 0; e < 8; ++e) v[e] += bv[e];
+        if (act == ACT_GELU) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[e] = gelu_erf(v[e]);
+        } else if (act == ACT_QUICKGELU) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[e] = quick_gelu(v[e]);
         }
-        if (a.resid) v += a.resid[(long)m * a.ldr + n];
+        if (a.pos) {
+          const int pr = a.pos_idx ? a.pos_idx[m] : m % a.pos_period;
+          const long pi = (long)pr * a.ld_pos + n;
+          if (a.pos_f32) {
+            const float4 p0 = *reinterpret_cast<const float4*>(static_cast<const float*>(a.pos) + pi);
+            const float4 p1 = *reinterpret_cast<const float4*>(static_cast<const float*>(a.pos) + pi + 4);
+            v[0] += p0.x; v[1] += p0.y; v[2] += p0.z; v[3] += p0.w;
+            v[4] += p1.x; v[5] += p1.y; v[6] += p1.z; v[7] += p1.w;
+          } else {
+            union { uint4 u; bf16 h[8]; } pb;
+            pb.u = *reinterpret_cast<const uint4*>(static_cast<const bf16*>(a.pos) + pi);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) v[e] += (float)pb.h[e];
+          }
+        }
+        if (a.resid) {
+          const float4 r0 = *reinterpret_cast<const float4*>(a.resid + (long)m * a.ldr + n);
+          const float4 r1 = *reinterpret_cast<const float4*>(a.resid + (long)m * a.ldr + n + 4);
+          v[0] += r0.x; v[1] += r0.y; v[2] += r0.z; v[3] += r0.w;
+          v[4] += r1.x; v[5] += r1.y; v[6] += r1.z; v[7] += r1.w;
+        }
         const long oi = (long)m * a.ldo + n;
-        if (a.out_f32) static_cast<float*>(a.out)[oi] = v;
-        else static_cast<bf16*>(a.out)[oi] = (bf16)v;
+        if (a.out_f32) {
+          float* o = static_cast<float*>(a.out) + oi;
+          *reinterpret_cast<float4*>(o) = make_float4(v[0], v[1], v[2], v[3]);
+          *reinterpret_cast<float4*>(o + 4) = make_float4(v[4], v[5], v[6], v[7]);
+        } else {
+          union { uint4 u; bf16 h[8]; } pk;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) pk.h[e] = (bf16)v[e];
+          *reinterpret_cast<uint4*>(static_cast<bf16*>(a.out) + oi) = pk.u;
+        }
       }
     }
+    wait_lds();
+    __builtin_amdgcn_wave_barrier();
   }
 }
 
-template <int BM, int BN, int WM, int WN, bool LN, bool GENERIC>
-hipError_t launch_cfg(const GemmArgs& a, hipStream_t s) {
+template <int BM, int BN, int WGM, int WGN>
+hipError_t launch_tile(const GemmArgs& a, hipStream_t s) {
+  using C = Cfg<BM, BN, WGM, WGN>;
+  static bool attr = false;   // raise the dynamic-LDS limit once per instantiation
+  if (!attr) {
+    const hipError_t e = hipFuncSetAttribute((const void*)gemm_bf16_tile_kernel<BM, BN, WGM, WGN>,
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
+    if (e != hipSuccess) return e;
+    attr = true;
+  }
   const long tiles = (long)((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
-  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN, LN, GENERIC>), dim3((unsigned)tiles),
-                     dim3(Tile<BM, BN, WM, WN>::NT), 0, s, a);
+  hipLaunchKernelGGL((gemm_bf16_tile_kernel<BM, BN, WGM, WGN>), dim3((unsigned)tiles), dim3(C::NT), C::LDS, s, a);
   return hipGetLastError();
+}
+
+bool al16(const void* p) { return (uintptr_t)p % 16 == 0; }
+
+// The DMA tile kernel's requirements: 16-byte aligned operand rows, K a
+// multiple of its k-step, 32-bit byte offsets, and 8-column epilogue chunks
+// with 16-byte aligned rows in every epilogue stream.
+bool tile_ok(const GemmArgs& a) {
+  if (a.stats || a.K % BK || a.N % 8 || a.lda % 8 || a.ldb % 8 || !al16(a.A) || !al16(a.B)) return false;
+  if ((double)a.M * a.lda * 2 >= 4294967296.0 || (double)a.N * a.ldb * 2 >= 4294967296.0) return false;
+  if (a.out_f32 ? (a.ldo % 4 != 0) : (a.ldo % 8 != 0)) return false;
+  if (!al16(a.out) || (a.resid && (a.ldr % 4 || !al16(a.resid)))) return false;
+  if (a.pos && (!al16(a.pos) || (a.pos_f32 ? a.ld_pos % 4 : a.ld_pos % 8))) return false;
+  return true;
 }
 
 }  // namespace
 
 hipError_t launch_gemm_bf16(const GemmArgs& a, hipStream_t s, const char** kname) {
-  const bool ln = a.stats != nullptr;
-  const bool aligned = (a.K % BK == 0) && (a.lda % 8 == 0) && (a.ldb % 8 == 0) &&
-                       ((uintptr_t)a.A % 16 == 0) && ((uintptr_t)a.B % 16 == 0) && (!ln || a.ln_dim % 8 == 0);
-  if (!aligned) {
-    if (ln) return hipErrorInvalidValue;   // LN prologue needs the aligned path
-    *kname = "gemm_bf16_generic_128x128";
-    return launch_cfg<128, 128, 64, 64, false, true>(a, s);
+  if (!tile_ok(a)) return launch_gemm_bf16_staged(a, s, kname);
+  // Pick the tile by estimated time: full-chip rounds (256 CUs; one 256-wide
+  // or two 128 x 128 workgroups per CU) times the tile's work over its
+  // measured relative efficiency.  All tiles sum k in the same order, so the
+  // choice never changes a result.
+  struct Opt { int bm, bn, per_cu; double eff; };
+  const Opt opts[3] = {{256, 256, 1, 1.00}, {256, 128, 1, 0.90}, {128, 128, 2, 0.85}};
+  int best = 0;
+  double best_t = 1e300;
+  for (int i = 0; i < 3; ++i) {
+    const long tiles = (long)((a.M + opts[i].bm - 1) / opts[i].bm) * ((a.N + opts[i].bn - 1) / opts[i].bn);
+    const long slots = 256L * opts[i].per_cu;
+    const double t = (double)((tiles + slots - 1) / slots) * opts[i].bm * opts[i].bn * opts[i].per_cu / opts[i].eff;
+    if (t < best_t) { best_t = t; best = i; }
   }
-  // Pick the tile by the number of full-chip rounds it needs (256 CUs; one
-  // 256x256 or two 128x128 workgroups per CU).  Both tiles accumulate k in
-  // the same order, so the choice never changes a result.
-  const long t256 = (long)((a.M + 255) / 256) * ((a.N + 255) / 256);
-  const long t128 = (long)((a.M + 127) / 128) * ((a.N + 127) / 128);
-  const long cost256 = ((t256 + 255) / 256) * 4, cost128 = ((t128 + 511) / 512) * 2;
-  const bool big = cost256 <= cost128;
-  if (ln) {   // the fp32 staging of the LN prologue does not fit a 256 x 256 tile's registers
-    *kname = "gemm_bf16_ln_128x128";
-    return launch_cfg<128, 128, 64, 64, true, false>(a, s);
+  switch (best) {
+    case 0: *kname = "gemm_bf16_256x256"; return launch_tile<256, 256, 2, 4>(a, s);
+    case 1: *kname = "gemm_bf16_256x128"; return launch_tile<256, 128, 4, 2>(a, s);
+    default: *kname = "gemm_bf16_128x128"; return launch_tile<128, 128, 2, 2>(a, s);
   }
-  *kname = big ? "gemm_bf16_256x256" : "gemm_bf16_128x128";
-  return big ? launch_cfg<256, 256, 128, 128, false, false>(a, s) : launch_cfg<128, 128, 64, 64, false, false>(a, s);
 }
 
 }  // namespace eas

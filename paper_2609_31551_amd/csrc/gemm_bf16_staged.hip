@@ -1,0 +1,242 @@
+// Register-staged bf16 MFMA GEMM: the path for operands the DMA-fed tile
+// kernel (gemm_bf16.hip) cannot take -- rows that are not 16-byte aligned or
+// K not a multiple of its k-step (the patch embedding, K = 588 / 1176) -- and
+// the LayerNorm-prologue form.  Same contract: C[m, n] = sum_k A[m, k] * B[n, k].
+//
+// Design (gfx950):
+//  * v_mfma_f32_32x32x16_bf16: each lane feeds 8 consecutive k of one row of
+//    A and of B straight from a 16-byte LDS read; fp32 accumulators.
+//  * Workgroup tile BM x BN, k-step 64; waves in a (BM/WM) x (BN/WN) grid,
+//    each a WM x WN sub-tile of (WM/32) x (WN/32) MFMA blocks: 256 x 256 with
+//    4 waves of 128 x 128 (accumulators in AGPRs), or 128 x 128 with 4 waves
+//    of 64 x 64.
+//  * Two LDS stages: the global loads of step k+1 are issued before the MFMAs
+//    of step k and written to the other stage after them, so one barrier per
+//    k-step suffices.  LDS rows are padded by 16 bytes so the 32 rows one
+//    16-byte read touches land on distinct banks.
+//  * LayerNorm prologue: with `stats`, A is the fp32 residual stream and the
+//    loader applies (x - mean) * rstd * g + b before rounding to bf16, so no
+//    normalised copy of the activations ever goes to HBM.
+//  * Fused epilogue: bias, GELU / QuickGELU, position-table add and fp32
+//    residual add, then one store (fp32 or bf16).  Accumulators go through
+//    LDS one 32-row slab per wave, so the residual reads and the output
+//    stores walk rows with the 64 lanes on consecutive columns.
+//  * Each output element accumulates k in the same order (16-wide MFMA
+//    steps, ascending) whatever the tile shape or M, so a request's result
+//    does not depend on what else is in the micro-batch.
+#include "common.h"
+
+namespace eas {
+namespace {
+
+constexpr int BK = 64;
+constexpr int LDK = BK + 8;   // padded LDS row (bf16 elements)
+
+template <int BM, int BN, int WM, int WN>
+struct Tile {
+  static constexpr int WAVES_N = BN / WN;
+  static constexpr int NT = 64 * (BM / WM) * (BN / WN);
+  static constexpr int FM = WM / 32, FN = WN / 32;
+  static constexpr int CPR = BK / 8;            // 8-element chunks per tile row
+  static constexpr int A_CH = BM * CPR / NT;    // A chunks per thread per stage
+  static constexpr int B_CH = BN * CPR / NT;
+  static constexpr int STAGE = (BM + BN) * LDK; // bf16 elements per LDS stage
+};
+
+__device__ __forceinline__ uint4 load16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
+
+// Bounds-checked 8-element load of row `r`, columns k..k+7 (zero outside).
+__device__ __forceinline__ uint4 load8_checked(const bf16* base, int ld, int r, int rows, int k, int K) {
+  union { uint4 u; bf16 h[8]; } v;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) v.h[e] = (r < rows && k + e < K) ? base[(long)r * ld + k + e] : (bf16)0.0f;
+  return v.u;
+}
+
+template <int BM, int BN, int WM, int WN, bool LN, bool GENERIC>
+__global__ __launch_bounds__(64 * (BM / WM) * (BN / WN)) void gemm_bf16_kernel(GemmArgs a) {
+  using T = Tile<BM, BN, WM, WN>;
+  __shared__ __attribute__((aligned(16))) bf16 smem[2 * T::STAGE];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / T::WAVES_N, wn = wave % T::WAVES_N;
+  const int tiles_n = (a.N + BN - 1) / BN;
+  const int m0 = (blockIdx.x / tiles_n) * BM, n0 = (blockIdx.x % tiles_n) * BN;
+  const int KT = (a.K + BK - 1) / BK;
+
+  const bf16* Ab = static_cast<const bf16*>(a.A);
+  const float* Af = static_cast<const float*>(a.A);
+  const bf16* Bb = static_cast<const bf16*>(a.B);
+
+  // staging registers for one stage
+  uint4 ra[LN ? 1 : T::A_CH];
+  float4 rf[LN ? 2 * T::A_CH : 1];
+  float2 rst[LN ? T::A_CH : 1];
+  uint4 rg, rb;
+  uint4 rbw[T::B_CH];
+
+  auto load_stage = [&](int kt) {
+    const int k0 = kt * BK;
+#pragma unroll
+    for (int i = 0; i < T::A_CH; ++i) {
+      const int c = tid + i * T::NT, row = c / T::CPR, kc = (c % T::CPR) * 8;
+      const int gm = m0 + row, gk = k0 + kc;
+      if constexpr (LN) {
+        const int r = gm < a.M ? gm : a.M - 1;
+        const float* p = Af + (long)r * a.lda + gk;
+        rf[2 * i] = *reinterpret_cast<const float4*>(p);
+        rf[2 * i + 1] = *reinterpret_cast<const float4*>(p + 4);
+        rst[i] = a.stats[(long)r * a.ln_group + gk / a.ln_dim];
+        if (i == 0) {
+          const int kk = gk % a.ln_dim;
+          rg = load16(static_cast<const bf16*>(a.ln_g) + kk);
+          rb = load16(static_cast<const bf16*>(a.ln_b) + kk);
+        }
+      } else if constexpr (GENERIC) {
+        ra[i] = load8_checked(Ab, a.lda, gm, a.M, gk, a.K);
+      } else {
+        const int r = gm < a.M ? gm : a.M - 1;
+        ra[i] = load16(Ab + (long)r * a.lda + gk);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < T::B_CH; ++i) {
+      const int c = tid + i * T::NT, row = c / T::CPR, kc = (c % T::CPR) * 8;
+      const int gn = n0 + row, gk = k0 + kc;
+      if constexpr (GENERIC) {
+        rbw[i] = load8_checked(Bb, a.ldb, gn, a.N, gk, a.K);
+      } else {
+        const int r = gn < a.N ? gn : a.N - 1;
+        rbw[i] = load16(Bb + (long)r * a.ldb + gk);
+      }
+    }
+  };
+
+  auto store_stage = [&](int buf) {
+    bf16* As = smem + buf * T::STAGE;
+    bf16* Bs = As + BM * LDK;
+#pragma unroll
+    for (int i = 0; i < T::A_CH; ++i) {
+      const int c = tid + i * T::NT, row = c / T::CPR, kc = (c % T::CPR) * 8;
+      if constexpr (LN) {
+        union { uint4 u; bf16 h[8]; } g, b, o;
+        g.u = rg; b.u = rb;
+        const float x[8] = {rf[2 * i].x, rf[2 * i].y, rf[2 * i].z, rf[2 * i].w,
+                            rf[2 * i + 1].x, rf[2 * i + 1].y, rf[2 * i + 1].z, rf[2 * i + 1].w};
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          o.h[e] = (bf16)((x[e] - rst[i].x) * rst[i].y * (float)g.h[e] + (float)b.h[e]);
+        *reinterpret_cast<uint4*>(As + row * LDK + kc) = o.u;
+      } else {
+        *reinterpret_cast<uint4*>(As + row * LDK + kc) = ra[i];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < T::B_CH; ++i) {
+      const int c = tid + i * T::NT, row = c / T::CPR, kc = (c % T::CPR) * 8;
+      *reinterpret_cast<uint4*>(Bs + row * LDK + kc) = rbw[i];
+    }
+  };
+
+  f32x16 acc[T::FM][T::FN];
+#pragma unroll
+  for (int i = 0; i < T::FM; ++i)
+#pragma unroll
+    for (int j = 0; j < T::FN; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+
+  load_stage(0);
+  store_stage(0);
+  __syncthreads();
+
+  const int lrow = lane & 31, lk = (lane >> 5) * 8;
+  for (int kt = 0; kt < KT; ++kt) {
+    const int cur = kt & 1;
+    if (kt + 1 < KT) load_stage(kt + 1);
+    const bf16* As = smem + cur * T::STAGE;
+    const bf16* Bs = As + BM * LDK;
+#pragma unroll
+    for (int ks = 0; ks < BK / 16; ++ks) {
+      bf16x8 af[T::FM], bfg[T::FN];
+#pragma unroll
+      for (int i = 0; i < T::FM; ++i)
+        af[i] = *reinterpret_cast<const bf16x8*>(As + (wm * WM + i * 32 + lrow) * LDK + ks * 16 + lk);
+#pragma unroll
+      for (int j = 0; j < T::FN; ++j)
+        bfg[j] = *reinterpret_cast<const bf16x8*>(Bs + (wn * WN + j * 32 + lrow) * LDK + ks * 16 + lk);
+#pragma unroll
+      for (int i = 0; i < T::FM; ++i)
+#pragma unroll
+        for (int j = 0; j < T::FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfg[j], acc[i][j], 0, 0, 0);
+    }
+    if (kt + 1 < KT) store_stage(cur ^ 1);
+    __syncthreads();
+  }
+
+  // ---- fused epilogue, staged through LDS one 32-row slab per wave ----
+  constexpr int SLD = WN + 4;   // padded slab row (floats)
+  float* slab = reinterpret_cast<float*>(smem) + wave * 32 * SLD;
+  const bf16* bias = static_cast<const bf16*>(a.bias);
+#pragma unroll
+  for (int i = 0; i < T::FM; ++i) {
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < T::FN; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e)
+        slab[((e >> 2) * 8 + (lane >> 5) * 4 + (e & 3)) * SLD + j * 32 + lrow] = acc[i][j][e];
+    __syncthreads();
+    const int mrow0 = m0 + wm * WM + i * 32;
+#pragma unroll 1
+    for (int r = 0; r < 32; ++r) {
+      const int m = mrow0 + r;
+      if (m >= a.M) break;
+      const int pr = a.pos ? (a.pos_idx ? a.pos_idx[m] : m % a.pos_period) : 0;
+#pragma unroll
+      for (int c = lane; c < WN; c += 64) {
+        const int n = n0 + wn * WN + c;
+        if (n >= a.N) continue;
+        float v = apply_act(a.act, slab[r * SLD + c] + (bias ? (float)bias[n] : 0.0f));
+        if (a.pos) {
+          const long pi = (long)pr * a.ld_pos + n;
+          v += a.pos_f32 ? static_cast<const float*>(a.pos)[pi] : (float)static_cast<const bf16*>(a.pos)[pi];
+        }
+        if (a.resid) v += a.resid[(long)m * a.ldr + n];
+        const long oi = (long)m * a.ldo + n;
+        if (a.out_f32) static_cast<float*>(a.out)[oi] = v;
+        else static_cast<bf16*>(a.out)[oi] = (bf16)v;
+      }
+    }
+  }
+}
+
+template <int BM, int BN, int WM, int WN, bool LN, bool GENERIC>
+hipError_t launch_cfg(const GemmArgs& a, hipStream_t s) {
+  const long tiles = (long)((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
+  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN, LN, GENERIC>), dim3((unsigned)tiles),
+                     dim3(Tile<BM, BN, WM, WN>::NT), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_gemm_bf16_staged(const GemmArgs& a, hipStream_t s, const char** kname) {
+  const bool ln = a.stats != nullptr;
+  const bool aligned = (a.K % BK == 0) && (a.lda % 8 == 0) && (a.ldb % 8 == 0) &&
+                       ((uintptr_t)a.A % 16 == 0) && ((uintptr_t)a.B % 16 == 0) && (!ln || a.ln_dim % 8 == 0);
+  if (!aligned) {
+    if (ln) return hipErrorInvalidValue;   // the LN prologue needs the aligned path
+    *kname = "gemm_bf16_generic_128x128";
+    return launch_cfg<128, 128, 64, 64, false, true>(a, s);
+  }
+  if (ln) {
+    *kname = "gemm_bf16_ln_128x128";
+    return launch_cfg<128, 128, 64, 64, true, false>(a, s);
+  }
+  *kname = "gemm_bf16_staged_128x128";
+  return launch_cfg<128, 128, 64, 64, false, false>(a, s);
+}
+
+}  // namespace eas
