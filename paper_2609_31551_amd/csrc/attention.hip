@@ -233,12 +233,13 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a, AttnWork w) {
 
 int attention_q_tile(int dtype_bf16) { return dtype_bf16 ? QT : QT32; }
 
-hipError_t launch_attention_bf16(const AttnArgs& a, const AttnWork& w, int total_tiles, hipStream_t s,
+hipError_t launch_attention_bf16(const AttnArgs& a, const AttnWork& w, int total_tiles, int N, hipStream_t s,
                                  const char** kname) {
+  if (attention_dma_supported(a, N)) return launch_attention_bf16_dma(a, w, total_tiles, s, kname);
   const dim3 grid((unsigned)(total_tiles * a.heads)), blk(256);
   switch (a.hd) {
-    case 64: *kname = "attn_bf16_hd64"; hipLaunchKernelGGL((attn_bf16_kernel<64>), grid, blk, 0, s, a, w); break;
-    case 80: *kname = "attn_bf16_hd80"; hipLaunchKernelGGL((attn_bf16_kernel<80>), grid, blk, 0, s, a, w); break;
+    case 64: *kname = "attn_bf16_staged_hd64"; hipLaunchKernelGGL((attn_bf16_kernel<64>), grid, blk, 0, s, a, w); break;
+    case 80: *kname = "attn_bf16_staged_hd80"; hipLaunchKernelGGL((attn_bf16_kernel<80>), grid, blk, 0, s, a, w); break;
     case 128: *kname = "attn_bf16_hd128"; hipLaunchKernelGGL((attn_bf16_kernel<128>), grid, blk, 0, s, a, w); break;
     case 16: *kname = "attn_bf16_hd16"; hipLaunchKernelGGL((attn_bf16_kernel<16>), grid, blk, 0, s, a, w); break;
     case 32: *kname = "attn_bf16_hd32"; hipLaunchKernelGGL((attn_bf16_kernel<32>), grid, blk, 0, s, a, w); break;

@@ -1,0 +1,277 @@
+// Variable-length block-diagonal attention, bf16 MFMA, head_dim 64 or 80 --
+// the form that carries the CLIP, Qwen-ViT and Whisper encoders.
+//
+// For every sequence r (tokens cu[r] .. cu[r+1]) and head h:
+//   O = softmax(Q K^T / sqrt(hd)) V, full within the sequence, nothing across.
+//
+// Design (gfx950):
+//  * A workgroup is 2 waves and owns 128 queries of one (sequence, head);
+//    each wave owns 64 queries as two 32-query MFMA column blocks, so every
+//    K / V operand fragment read from LDS feeds two MFMAs.
+//  * K and V tiles of 64 keys arrive by direct DMA (global_load_lds_dwordx4)
+//    into two LDS buffers: tile t+1 streams in while tile t is consumed,
+//    one barrier per tile.  Tiles are anchored at the sequence start; rows
+//    past its end re-read the last row and are masked out of the softmax.
+//  * Both tiles are stored row-major with a per-row rotation of the 16-byte
+//    chunks (2(r&3) + ((r>>2)&1) for 8-chunk rows, (r>>2)&1 for 10-chunk
+//    rows) that keeps both access patterns below free of bank conflicts.
+//  * S^T = K Q^T (K rows as the A operand, Q in registers as the B operand):
+//    lane l holds 16 scores of query l % 32, so the online softmax is
+//    lane-local except one cross-half shuffle for the running max.
+//  * O^T += V^T P^T: the bf16-rounded probabilities already sit in the B
+//    operand layout; the V^T operand comes straight from the row-major V
+//    tile through ds_read_b64_tr_b16, whose 16-lane transpose turns four
+//    8-byte row pieces into four columns.
+//  * A 32-key half tile that lies wholly past the sequence end is skipped,
+//    and a wave whose queries all lie past the end skips the arithmetic.
+#include "common.h"
+
+namespace eas {
+namespace {
+
+constexpr int QTILE = 128, KTILE = 64;
+
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void dma16(unsigned lds_addr, unsigned voff, const void* gbase) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2\n"
+               :: "s"(lds_addr), "v"(voff), "s"(gbase) : "memory", "m0");
+}
+
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+
+template <int HD>
+struct AttnCfg {
+  static constexpr int R = HD / 8;                 // 16-byte chunks per K / V row
+  static constexpr int KS = HD / 16;               // 16-wide k-steps of Q K^T
+  static constexpr int HB = (HD + 31) / 32;        // 32-row blocks of O^T
+  static constexpr int TILE = KTILE * R * 16;      // bytes of one K or V tile
+  static constexpr int BUF = 2 * TILE;             // K + V
+  static constexpr int DMA = R / 2;                // DMA instructions per wave per operand per tile
+  __device__ static int rot(int row) { return R == 8 ? 2 * (row & 3) + ((row >> 2) & 1) : ((row >> 2) & 1); }
+  __device__ static int phys(int row, int L) { return (L + rot(row)) % R; }
+  __device__ static int logical(int row, int p) { return (p + R - rot(row)) % R; }
+};
+
+__device__ __forceinline__ void decode(const AttnWork& w, int tile, int* s0, int* s1, int* q0) {
+  int i = 0;
+  while (i + 1 < w.n && w.tile_start[i + 1] <= tile) ++i;
+  const int r = w.order[i];
+  *s0 = w.cu[r];
+  *s1 = w.cu[r + 1];
+  *q0 = *s0 + (tile - w.tile_start[i]) * QTILE;
+}
+
+template <int HD>
+__global__ __launch_bounds__(128) void attn_bf16_dma_kernel(AttnArgs a, AttnWork w) {
+  using C = AttnCfg<HD>;
+  extern __shared__ __attribute__((aligned(1024))) char smem[];
+  const unsigned lds0 = (unsigned)(size_t)((__attribute__((address_space(3))) char*)smem);
+  const int h = blockIdx.x % a.heads;
+  int s0, s1, q0;
+  decode(w, blockIdx.x / a.heads, &s0, &s1, &q0);
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int g = lane >> 5, l32 = lane & 31;
+  const int dq = a.heads * HD;
+  const bf16* qkv = static_cast<const bf16*>(a.qkv);
+  const float c = a.scale * 1.4426950408889634f;
+  const int qw0 = q0 + wave * 64;            // this wave's first query
+  const bool active = qw0 < s1;              // uniform per wave
+
+  // ---- DMA of one K + V tile: wave w moves K and V chunks [w*DMA*64, (w+1)*DMA*64) ----
+  // slot s of a tile is 16 bytes at s*16: row s / R, physical chunk s % R.
+  int drow[C::DMA], dcol[C::DMA];
+#pragma unroll
+  for (int j = 0; j < C::DMA; ++j) {
+    const int slot = (wave * C::DMA + j) * 64 + lane;
+    drow[j] = slot / C::R;
+    dcol[j] = h * HD + C::logical(drow[j], slot % C::R) * 8;
+  }
+  auto issue = [&](int k0, int buf) {
+    const unsigned base = lds0 + buf * C::BUF;
+#pragma unroll
+    for (int j = 0; j < C::DMA; ++j) {
+      const int key = min(k0 + drow[j], s1 - 1);
+      const unsigned off = (unsigned)(((long)key * a.ldqkv + dcol[j]) * 2);
+      dma16(base + (wave * C::DMA + j) * 1024, off + dq * 2, qkv);               // K
+      dma16(base + C::TILE + (wave * C::DMA + j) * 1024, off + 2 * dq * 2, qkv); // V
+    }
+  };
+
+  // Q fragments: query block qb, k-step ks: lane l holds hd ks*16 + g*8 .. +8 of query l%32
+  bf16x8 qf[2][C::KS];
+#pragma unroll
+  for (int qb = 0; qb < 2; ++qb) {
+    const int qr = min(qw0 + qb * 32 + l32, s1 - 1);
+#pragma unroll
+    for (int ks = 0; ks < C::KS; ++ks)
+      qf[qb][ks] = *reinterpret_cast<const bf16x8*>(qkv + (long)qr * a.ldqkv + h * HD + ks * 16 + g * 8);
+  }
+  // consume the Q loads here, before any DMA is in flight, so the compiler's
+  // own wait for them cannot also wait on a prefetch
+#pragma unroll
+  for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+    for (int ks = 0; ks < C::KS; ++ks) asm volatile("" :: "v"(qf[qb][ks]));
+
+  f32x16 o[2][C::HB];
+#pragma unroll
+  for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+    for (int hb = 0; hb < C::HB; ++hb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) o[qb][hb][e] = 0.0f;
+  float m_run[2] = {-INFINITY, -INFINITY}, l_part[2] = {0.0f, 0.0f};
+
+  // K operand reads: row kb*32 + l32, logical chunk 2ks + g (the rotation only
+  // depends on row & 7, i.e. on l32)
+  int kofs[C::KS];
+#pragma unroll
+  for (int ks = 0; ks < C::KS; ++ks) kofs[ks] = l32 * C::R * 16 + C::phys(l32, 2 * ks + g) * 16;
+  // V^T operand reads: lane 16q + 4e + t reads row 32kb + 16ch + 8half + 4g + e,
+  // columns hb*32 + 16(q%2) + 4t .. +4; the row's rotation depends only on (g, e)
+  const int vq = lane >> 4, ve = (lane >> 2) & 3, vt = lane & 3;
+  const int vrow = 4 * g + ve;
+  int vofs[C::HB];
+#pragma unroll
+  for (int hb = 0; hb < C::HB; ++hb) {
+    int col = hb * 32 + 16 * (vq & 1) + 4 * vt;
+    if (col >= HD) col -= 16;   // padding rows of the last O^T block: any real column, result dropped
+    vofs[hb] = vrow * C::R * 16 + C::phys(vrow, col >> 3) * 16 + (col & 7) * 2;
+  }
+  __attribute__((address_space(3))) char* lds = (__attribute__((address_space(3))) char*)smem;
+
+  const int ntiles = (s1 - s0 + KTILE - 1) / KTILE;
+  issue(s0, 0);
+  for (int t = 0; t < ntiles; ++t) {
+    const int k0 = s0 + t * KTILE, buf = t & 1;
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");   // tile t landed; reads of t-1 done
+    __syncthreads();
+    if (t + 1 < ntiles) issue(k0 + KTILE, buf ^ 1);
+    if (!active) continue;
+    const char* Kt = smem + buf * C::BUF;
+    const int nkb = k0 + 32 < s1 ? 2 : 1;   // 32-key halves holding at least one key
+
+    // the tile as two 32-key halves: S^T half -> softmax -> O^T update, so only
+    // one half's scores are live at a time
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      if (kb >= nkb) break;
+      f32x16 sc[2];
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) sc[qb][e] = 0.0f;
+#pragma unroll
+      for (int ks = 0; ks < C::KS; ++ks) {
+        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(Kt + kb * 32 * C::R * 16 + kofs[ks]);
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb)
+          sc[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[qb][ks], sc[qb], 0, 0, 0);
+      }
+      // Online softmax.  Scores are masked only in a half that reaches past the
+      // sequence end.  The running max m (log2 units, scale folded in) is raised
+      // lazily: O and the row sum keep a stale m until a lane's max exceeds it
+      // by more than 8, so p = 2^(s*c - m) <= 256 and the rescale of O is
+      // usually skipped; both share m, so O / sum is unchanged.
+      const int kh = k0 + kb * 32;
+      if (kh + 32 > s1) {
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+          for (int e = 0; e < 16; ++e)
+            if (kh + (e >> 2) * 8 + g * 4 + (e & 3) >= s1) sc[qb][e] = -INFINITY;
+      }
+      bf16x8 pb[2][2];
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb) {
+        float mx = sc[qb][0];
+#pragma unroll
+        for (int e = 1; e < 16; ++e) mx = fmaxf(mx, sc[qb][e]);
+        mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * c;
+        const bool need = mx > m_run[qb] + 8.0f;
+        if (__any(need)) {
+          const float m_new = need ? fmaxf(m_run[qb], mx) : m_run[qb];
+          const float alpha = __builtin_amdgcn_exp2f(m_run[qb] - m_new);
+          m_run[qb] = m_new;
+          l_part[qb] *= alpha;
+#pragma unroll
+          for (int hb = 0; hb < C::HB; ++hb)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) o[qb][hb][e] *= alpha;
+        }
+        const float nm = -m_run[qb];
+        float psum = 0.0f;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const float p = __builtin_amdgcn_exp2f(fmaf(sc[qb][e], c, nm));
+          psum += p;
+          pb[qb][e >> 3][e & 7] = (bf16)p;
+        }
+        l_part[qb] += psum;
+      }
+      // O^T += V^T P^T, 16 keys per MFMA
+#pragma unroll
+      for (int ch = 0; ch < 2; ++ch) {
+#pragma unroll
+        for (int hb = 0; hb < C::HB; ++hb) {
+          union { bf16x8 v; v4i16 h[2]; } va;
+#pragma unroll
+          for (int half = 0; half < 2; ++half) {
+            const int rbase = (kb * 32 + 16 * ch + 8 * half) * C::R * 16;
+            va.h[half] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (lds_v4i16*)(lds + buf * C::BUF + C::TILE + rbase + vofs[hb]));
+          }
+#pragma unroll
+          for (int qb = 0; qb < 2; ++qb)
+            o[qb][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va.v, pb[qb][ch], o[qb][hb], 0, 0, 0);
+        }
+      }
+    }
+  }
+
+  if (!active) return;
+#pragma unroll
+  for (int qb = 0; qb < 2; ++qb) {
+    const int qi = qw0 + qb * 32 + l32;
+    if (qi >= s1) continue;
+    const float inv = 1.0f / (l_part[qb] + __shfl_xor(l_part[qb], 32, 64));
+    bf16* out = static_cast<bf16*>(a.out) + (long)qi * a.ldo + h * HD;
+#pragma unroll
+    for (int hb = 0; hb < C::HB; ++hb)
+#pragma unroll
+      for (int e4 = 0; e4 < 4; ++e4) {
+        const int d = hb * 32 + e4 * 8 + g * 4;
+        if (d < HD) {
+          union { uint2 u; bf16 h[4]; } st;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) st.h[e] = (bf16)(o[qb][hb][e4 * 4 + e] * inv);
+          *reinterpret_cast<uint2*>(out + d) = st.u;
+        }
+      }
+  }
+}
+
+template <int HD>
+hipError_t launch_hd(const AttnArgs& a, const AttnWork& w, int total_tiles, hipStream_t s) {
+  constexpr int lds = 2 * AttnCfg<HD>::BUF;
+  hipLaunchKernelGGL((attn_bf16_dma_kernel<HD>), dim3((unsigned)(total_tiles * a.heads)), dim3(128), lds, s, a, w);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+bool attention_dma_supported(const AttnArgs& a, int N) {
+  return (a.hd == 64 || a.hd == 80) && a.ldqkv % 8 == 0 && (uintptr_t)a.qkv % 16 == 0 &&
+         (double)N * a.ldqkv * 2 < 4294967296.0;
+}
+
+hipError_t launch_attention_bf16_dma(const AttnArgs& a, const AttnWork& w, int total_tiles, hipStream_t s,
+                                     const char** kname) {
+  if (a.hd == 64) { *kname = "attn_bf16_hd64"; return launch_hd<64>(a, w, total_tiles, s); }
+  if (a.hd == 80) { *kname = "attn_bf16_hd80"; return launch_hd<80>(a, w, total_tiles, s); }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace eas

@@ -84,8 +84,12 @@ struct AttnArgs {
   int heads, hd;
   float scale;                     // 1 / sqrt(hd)
 };
-hipError_t launch_attention_bf16(const AttnArgs& a, const AttnWork& w, int total_tiles, hipStream_t s,
+hipError_t launch_attention_bf16(const AttnArgs& a, const AttnWork& w, int total_tiles, int N, hipStream_t s,
                                  const char** kname);
+// DMA-fed kernel for head_dim 64 / 80 (same 128-query tiles as the staged one)
+bool attention_dma_supported(const AttnArgs& a, int N);
+hipError_t launch_attention_bf16_dma(const AttnArgs& a, const AttnWork& w, int total_tiles, hipStream_t s,
+                                     const char** kname);
 hipError_t launch_attention_f32(const AttnArgs& a, const AttnWork& w, int total_tiles, hipStream_t s,
                                 const char** kname);
 int attention_q_tile(int dtype_bf16);

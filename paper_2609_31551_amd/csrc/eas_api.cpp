@@ -713,7 +713,7 @@ eas_status eas_encode_microbatch(eas_encoder* enc, const void* packed_in, const 
     aa.hd = hd;
     aa.scale = (float)(1.0 / std::sqrt((double)hd));
     EAS_TRY(run(enc, s, attn_flops, (double)N * 4 * d * el, [&](const char** kn) {
-      return bf ? launch_attention_bf16(aa, work, tiles, s, kn) : launch_attention_f32(aa, work, tiles, s, kn);
+      return bf ? launch_attention_bf16(aa, work, tiles, N, s, kn) : launch_attention_f32(aa, work, tiles, s, kn);
     }));
     GemmArgs go = gemm_args(N, d, d, enc->ao, d, W(p + "o.w"), d, enc->x, d, 1);
     go.bias = W(p + "o.b");
