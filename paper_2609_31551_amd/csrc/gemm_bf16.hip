@@ -5,19 +5,21 @@
 //
 // Design (gfx950, one workgroup per BM x BN output tile):
 //  * Operands reach LDS by direct DMA: global_load_lds_dwordx4 moves 16 bytes
-//    per lane from HBM/L2 into LDS without passing through VGPRs.  One wave
-//    instruction fills 1 KB = 16 rows x 64 bytes (a 32-wide k-slice of bf16).
-//    The lane -> (row, 16-byte chunk) assignment applies an XOR swizzle
-//    (chunk ^ ((row >> 1) & 3)) so that the MFMA operand reads, 32 rows at a
-//    time at one k offset, spread over all LDS banks.
-//  * k-step 32, 4 LDS stages: tile k+3 is in flight while tile k is
-//    consumed.  The DMA is issued from inline assembly so the compiler does
-//    not serialise it against the LDS reads; completion is tracked with
-//    explicit s_waitcnt vmcnt and one workgroup barrier per k-step.
+//    per lane from HBM/L2 into LDS without passing through VGPRs.  With a
+//    64-wide k-step one wave instruction fills 1 KB = 8 rows x 128 bytes, so
+//    every lane group reads whole 128-byte lines.  The lane -> (row, 16-byte
+//    chunk) assignment applies an XOR swizzle (chunk ^ ((row >> 1) & 7)) that
+//    spreads the MFMA operand reads -- 32 rows at one k offset, 16 lanes per
+//    LDS cycle over 64 banks -- without conflicts.
+//  * Two LDS stages of 64 k: tile k+1 streams in while tile k is consumed.
+//    The DMA is issued from inline assembly so the compiler does not
+//    serialise it against the LDS reads; completion is tracked with explicit
+//    s_waitcnt vmcnt and one workgroup barrier per k-step.
 //  * v_mfma_f32_32x32x16_bf16, each wave a (BM/WGM) x (BN/WGN) sub-tile of
-//    32 x 32 blocks; operand fragments for the second 16-wide half of a
-//    k-step are read while the first half's MFMAs run, and the barrier sits
-//    between the halves so its wait overlaps queued MFMAs.
+//    32 x 32 blocks (8 waves of 64 x 128 for the 256 x 256 tile); operand
+//    fragments for the next 16-wide k slice are read while the current
+//    slice's MFMAs run, and the barrier sits before the last slice so its
+//    wait overlaps queued MFMAs.
 //  * Tiles are handed out XCD-aware: workgroups are dispatched round-robin
 //    over the 8 XCDs, so block b is remapped to give every XCD a contiguous
 //    run of output tiles that share A row panels in that XCD's L2.
@@ -25,15 +27,15 @@
 //    accumulators, then every lane owns 8 consecutive columns of a row and
 //    applies bias, GELU / QuickGELU, a position-table row and the fp32
 //    residual before one 16-byte (bf16) or 2 x 16-byte (fp32) store.
-//  * Every output element accumulates k in the same order (32-wide k-steps,
-//    two 16-wide MFMA halves, ascending) whatever the tile shape or M, so a
+//  * Every output element accumulates k in the same order (16-wide MFMA
+//    slices, ascending) whatever the tile shape or M, so a
 //    request's result does not depend on what else is in the micro-batch.
 #include "common.h"
 
 namespace eas {
 namespace {
 
-constexpr int BK = 32, ST = 4;
+constexpr int BK = 64, ST = 2;
 
 // M0 carries the LDS base of each DMA; nothing else in these kernels uses M0
 // (checked in the generated code), so setting it here cannot disturb the
@@ -55,12 +57,16 @@ struct Cfg {
   static constexpr int WM = BM / WGM, WN = BN / WGN;
   static constexpr int FM = WM / 32, FN = WN / 32;
   static constexpr int TA = BM * BK * 2, TB = BN * BK * 2, STAGE = TA + TB;
-  static constexpr int DA = BM / 16 / NW, DB = BN / 16 / NW;   // DMA instructions per wave per stage
+  static constexpr int RPI = 1024 / (BK * 2);                   // rows per DMA instruction
+  static constexpr int CPR = BK / 8;                            // 16-byte chunks per row
+  static constexpr int DA = BM / RPI / NW, DB = BN / RPI / NW;   // DMA instructions per wave per stage
   static constexpr int DPS = DA + DB;
   static constexpr int SLD = WN + 4;                            // epilogue slab row (floats)
   static constexpr int LDS = ST * STAGE > NW * 32 * SLD * 4 ? ST * STAGE : NW * 32 * SLD * 4;
-  static_assert(BM % (16 * NW) == 0 && BN % (16 * NW) == 0, "DMA split");
-  static_assert(3 * DPS < 64, "vmcnt range");
+  static_assert(BM % (RPI * NW) == 0 && BN % (RPI * NW) == 0, "DMA split");
+  static_assert(DPS < 64, "vmcnt range");
+  // conflict-free chunk swizzle for 128-byte rows: 16 rows per LDS cycle hit 16 distinct 16-byte slots
+  __device__ static int sw(int row) { return (row >> 1) & 7; }
 };
 
 // XCD-aware block -> tile index (bijective on [0, nb)).
@@ -85,21 +91,23 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_tile_kernel(GemmArgs
   const bf16* A = static_cast<const bf16*>(a.A);
   const bf16* B = static_cast<const bf16*>(a.B);
 
-  // DMA sources: instruction j of this wave fills tile rows (wave*D + j)*16 .. +16;
-  // lane i -> row +i/4, physical chunk i%4 holding logical chunk (i%4) ^ ((row>>1)&3).
+  // DMA sources: instruction j of this wave fills tile rows (wave*D + j)*8 .. +8;
+  // lane i -> row +i/8, physical chunk i%8 holding logical chunk (i%8) ^ sw(row).
   // Rows past M or N re-read the last row; their results are never stored.
   unsigned a_off[C::DA], b_off[C::DB];
   {
-    const int c = (lane & 3) ^ ((lane >> 3) & 3);
+    const int rr = lane / C::CPR, pch = lane % C::CPR;
 #pragma unroll
     for (int j = 0; j < C::DA; ++j) {
-      const int gm = min(m0 + (wave * C::DA + j) * 16 + (lane >> 2), a.M - 1);
-      a_off[j] = (unsigned)(((long)gm * a.lda + c * 8) * 2);
+      const int r = (wave * C::DA + j) * C::RPI + rr;
+      const int gm = min(m0 + r, a.M - 1);
+      a_off[j] = (unsigned)(((long)gm * a.lda + (pch ^ C::sw(r)) * 8) * 2);
     }
 #pragma unroll
     for (int j = 0; j < C::DB; ++j) {
-      const int gn = min(n0 + (wave * C::DB + j) * 16 + (lane >> 2), a.N - 1);
-      b_off[j] = (unsigned)(((long)gn * a.ldb + c * 8) * 2);
+      const int r = (wave * C::DB + j) * C::RPI + rr;
+      const int gn = min(n0 + r, a.N - 1);
+      b_off[j] = (unsigned)(((long)gn * a.ldb + (pch ^ C::sw(r)) * 8) * 2);
     }
   }
   auto issue = [&](int kt, int st) {
@@ -112,11 +120,14 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_tile_kernel(GemmArgs
     for (int j = 0; j < C::DB; ++j) dma16(base + C::TA + (wave * C::DB + j) * 1024, b_off[j], gb);
   };
 
-  // operand fragment addresses: row wm*WM + i*32 + lane%32, logical chunk 2*half + lane/32
-  const int lrow = lane & 31, g = lane >> 5, sw = (lrow >> 1) & 3;
-  const int a_row = (wm * C::WM + lrow) * 64, b_row = (wn * C::WN + lrow) * 64;
-  const int cofs0 = ((0 + g) ^ sw) << 4, cofs1 = ((2 + g) ^ sw) << 4;
-
+  // operand fragment reads: row wm*WM + i*32 + lane%32, logical chunk 2*slice + lane/32;
+  // the swizzle only depends on the row's low bits, i.e. on lane%32
+  const int lrow = lane & 31, g = lane >> 5, swz = C::sw(lrow);
+  const int a_row = (wm * C::WM + lrow) * BK * 2, b_row = (wn * C::WN + lrow) * BK * 2;
+  constexpr int NH = BK / 16;   // 16-wide k slices per k-step
+  int cofs[NH];
+#pragma unroll
+  for (int h = 0; h < NH; ++h) cofs[h] = ((2 * h + g) ^ swz) << 4;
   f32x16 acc[C::FM][C::FN];
 #pragma unroll
   for (int i = 0; i < C::FM; ++i)
@@ -125,14 +136,14 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_tile_kernel(GemmArgs
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
 
-  bf16x8 fa0[C::FM], fb0[C::FN], fa1[C::FM], fb1[C::FN];
+  bf16x8 fa[2][C::FM], fb[2][C::FN];
   auto load_frags = [&](int st, int cofs, bf16x8* fa, bf16x8* fb) {
     const char* As = smem + st * C::STAGE;
     const char* Bs = As + C::TA;
 #pragma unroll
-    for (int i = 0; i < C::FM; ++i) fa[i] = *reinterpret_cast<const bf16x8*>(As + a_row + i * 32 * 64 + cofs);
+    for (int i = 0; i < C::FM; ++i) fa[i] = *reinterpret_cast<const bf16x8*>(As + a_row + i * 32 * BK * 2 + cofs);
 #pragma unroll
-    for (int j = 0; j < C::FN; ++j) fb[j] = *reinterpret_cast<const bf16x8*>(Bs + b_row + j * 32 * 64 + cofs);
+    for (int j = 0; j < C::FN; ++j) fb[j] = *reinterpret_cast<const bf16x8*>(Bs + b_row + j * 32 * BK * 2 + cofs);
   };
   auto mma = [&](const bf16x8* fa, const bf16x8* fb) {
 #pragma unroll
@@ -146,34 +157,29 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_tile_kernel(GemmArgs
 #pragma unroll
   for (int s = 0; s < ST; ++s)
     if (s < KT) issue(s, s);
-  {
-    const int later = KT - 1 < ST - 1 ? KT - 1 : ST - 1;   // tiles issued after tile 0
-    if (later >= 3) wait_vm<3 * C::DPS>();
-    else if (later == 2) wait_vm<2 * C::DPS>();
-    else if (later == 1) wait_vm<C::DPS>();
-    else wait_vm<0>();
-  }
+  if (KT > 1) wait_vm<C::DPS>();   // ST == 2: tile 1 may still be in flight
+  else wait_vm<0>();
   __syncthreads();
-  load_frags(0, cofs0, fa0, fb0);
+  load_frags(0, cofs[0], fa[0], fb[0]);
 
   for (int kt = 0; kt < KT; ++kt) {
     const int st = kt % ST;
-    load_frags(st, cofs1, fa1, fb1);
-    mma(fa0, fb0);
+#pragma unroll
+    for (int h = 0; h < NH - 1; ++h) {
+      load_frags(st, cofs[h + 1], fa[(h + 1) & 1], fb[(h + 1) & 1]);
+      mma(fa[h & 1], fb[h & 1]);
+    }
     if (kt + 1 < KT) {
-      // this wave's reads of stage st are done once lgkmcnt drains; tile kt+1 has
-      // landed once at most the tiles issued after it are outstanding; after the
-      // barrier every wave is past stage st, which is refilled with tile kt+ST
+      // this wave's reads of stage st are done once lgkmcnt drains; tile kt+1
+      // (the newest DMA) has landed at vmcnt 0; after the barrier every wave
+      // is past stage st, which is refilled with tile kt+ST
       wait_lds();
-      const int later = KT - 2 - kt;
-      if (later >= 2) wait_vm<2 * C::DPS>();
-      else if (later == 1) wait_vm<C::DPS>();
-      else wait_vm<0>();
+      wait_vm<0>();
       __builtin_amdgcn_s_barrier();
       if (kt + ST < KT) issue(kt + ST, st);
-      load_frags((kt + 1) % ST, cofs0, fa0, fb0);
+      load_frags((kt + 1) % ST, cofs[0], fa[NH & 1], fb[NH & 1]);
     }
-    mma(fa1, fb1);
+    mma(fa[(NH - 1) & 1], fb[(NH - 1) & 1]);
   }
 
   // ---- fused epilogue: per wave, 32-row slabs of its WM x WN sub-tile through LDS ----
@@ -295,7 +301,7 @@ hipError_t launch_gemm_bf16(const GemmArgs& a, hipStream_t s, const char** kname
   // measured relative efficiency.  All tiles sum k in the same order, so the
   // choice never changes a result.
   struct Opt { int bm, bn, per_cu; double eff; };
-  const Opt opts[3] = {{256, 256, 1, 1.00}, {256, 128, 1, 0.90}, {128, 128, 2, 0.85}};
+  const Opt opts[3] = {{256, 256, 1, 1.00}, {256, 128, 1, 0.80}, {128, 128, 2, 0.65}};
   int best = 0;
   double best_t = 1e300;
   for (int i = 0; i < 3; ++i) {
@@ -305,7 +311,7 @@ hipError_t launch_gemm_bf16(const GemmArgs& a, hipStream_t s, const char** kname
     if (t < best_t) { best_t = t; best = i; }
   }
   switch (best) {
-    case 0: *kname = "gemm_bf16_256x256"; return launch_tile<256, 256, 2, 4>(a, s);
+    case 0: *kname = "gemm_bf16_256x256"; return launch_tile<256, 256, 4, 2>(a, s);
     case 1: *kname = "gemm_bf16_256x128"; return launch_tile<256, 128, 4, 2>(a, s);
     default: *kname = "gemm_bf16_128x128"; return launch_tile<128, 128, 2, 2>(a, s);
   }
