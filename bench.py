@@ -3,17 +3,24 @@
 A step is one pass of the whole Encode hot path over one micro-batch that is
 already resident in HBM: pack the raw requests into a padding-free batch, then
 run the encoder forward pass and connector (eas_pack_microbatch +
-eas_encode_microbatch).  The default workload is a micro-batch of 64 CLIP
+eas_encode_microbatch).  The headline workload is a micro-batch of 64 CLIP
 ViT-L/14-336 images (577 tokens each, bf16 weights N(0, 0.02), pixels U[0,1),
-seed 0), the image workload of the paper's Table 3; a sweep over micro-batch
-sizes 1, 8, 32 and 64 follows.  Prints ONE JSON line.
+seed 0), the image workload of the paper's Table 3.  Prints ONE JSON line.
+
+Besides the headline, every workload of the evaluation (section 5.1) is swept
+over micro-batch sizes on a fixed pool of requests: a pass walks the whole
+pool in consecutive micro-batches of size B, so every B encodes the same
+requests (CLIP: 64 images; variable-resolution Qwen2-VL-style images: 64
+images; video: 4 clips of 16 x 448 x 448; Whisper-style audio: 32 clips).
 
 Roofline: during a second pass over the same steps every kernel launch is
 bracketed by HIP events on the encoder's stream; the kernel with the largest
 total time is the dominant kernel, and its algorithmic flops per launch over
 its mean duration is compared with the bf16 dense MFMA peak.  The CPU
 baseline times the fp64 reference on a bounded sample (whole images, full
-depth) on the host cores.
+depth) on the host cores; per-workload reference timings at micro-batch 1
+run at reduced depth where the full depth would exceed the time budget, and
+say so.
 """
 import argparse
 import hashlib
@@ -38,7 +45,12 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--preset", default="clip_vit_l14_336")
     ap.add_argument("--batch", type=int, default=64)
-    ap.add_argument("--sweep", default="1,8,32,64", help="micro-batch sizes ('' to skip)")
+    ap.add_argument("--sweep", default="1,2,4,8,16,32,64", help="micro-batch sizes of the headline preset ('' to skip)")
+    ap.add_argument("--workloads", default="qwen2vl_vit_image:64:1,2,4,8,16,32;qwen2vl_vit_video:4:1,2,4;"
+                    "whisper_large_enc:32:1,2,4,8,16,32",
+                    help="other workloads swept as preset:pool:sizes;... ('' to skip)")
+    ap.add_argument("--cpu-configs-budget-s", type=float, default=8.0,
+                    help="per-workload time budget of the micro-batch-1 reference timings (0 to skip)")
     ap.add_argument("--sweep-steps", type=int, default=5)
     ap.add_argument("--cpu-budget-s", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -82,60 +94,78 @@ def source_sha():
 
 
 class Workload:
-    def __init__(self, preset, batch, seed=0):
+    """A pool of synthetic requests resident in HBM, walked in micro-batches."""
+
+    def __init__(self, preset, pool, max_batch, seed=0):
         import torch
         from paper_2609_31551_amd import eas, synth
-        self.preset, self.batch = preset, batch
+        self.preset, self.pool = preset, pool
         t0 = time.time()
         self.weights_host = synth.make_weights(preset, seed)
-        self.items_host = synth.make_items(preset, batch, seed)
+        self.items_host = synth.make_items(preset, pool, seed)
         self.gen_s = time.time() - t0
+        cfg = eas.make_config(preset, 1 << 30, 1)
         tchw = [list(a.shape) if a.ndim == 4 else [1, 1] + list(a.shape) for a in self.items_host]
-        cu, _, _, _ = eas.microbatch_shape(eas.make_config(preset, 1 << 30, batch), tchw)
-        self.tokens = int(cu[-1])
+        self.item_tokens = [int(eas.microbatch_shape(cfg, [t])[0][-1]) for t in tchw]
+        max_tokens = sum(sorted(self.item_tokens)[-max_batch:])
         self.stream = torch.cuda.Stream()
-        self.enc = eas.Encoder(preset, max_tokens=self.tokens, max_seqs=batch)
+        self.enc = eas.Encoder(preset, max_tokens=max_tokens, max_seqs=max_batch)
         self.wdev = eas.upload_weights(self.enc.cfg, self.weights_host)
         self.items = [torch.from_numpy(a).cuda() for a in self.items_host]
-        self.packed, self.cu, self.grid = self.enc.pack_microbatch(self.items, stream=self.stream)
-        self.grid_arg = None if preset["kind"] == "whisper" else self.grid
-        self.out = torch.empty((self.enc.out_rows(self.cu), preset["out_dim"]), dtype=torch.float32, device="cuda")
+        self.whisper = preset["kind"] == "whisper"
+        item_rows = [self.enc.out_rows([0, t]) for t in self.item_tokens]
+        rows = sum(sorted(item_rows)[-max_batch:])
+        self.out = torch.empty((rows, preset["out_dim"]), dtype=torch.float32, device="cuda")
         torch.cuda.synchronize()
 
-    def step(self, n):
-        """One pass over the first n requests: pack + encode."""
+    def step(self, start, n):
+        """Pack + encode requests [start, start + n)."""
         import torch
         with torch.cuda.stream(self.stream):
-            packed, cu, grid = self.enc.pack_microbatch(self.items[:n], stream=self.stream)
-            self.enc.encode_microbatch(packed, cu, grid if self.grid_arg is not None else None, self.wdev,
+            packed, cu, grid = self.enc.pack_microbatch(self.items[start:start + n], stream=self.stream)
+            self.enc.encode_microbatch(packed, cu, None if self.whisper else grid, self.wdev,
                                        out=self.out[:self.enc.out_rows(cu)], stream=self.stream)
         return int(cu[-1])
 
-    def time_steps(self, n, steps, warmup):
+    def run_pass(self, b, first=None):
+        """Consecutive micro-batches of b over the first `first` requests (default: the pool)."""
+        end = self.pool if first is None else first
+        tok = 0
+        for i in range(0, end, b):
+            tok += self.step(i, min(b, end - i))
+        return tok
+
+    def time_passes(self, b, reps, warmup, first=None):
         import torch
         for _ in range(warmup):
-            self.step(n)
+            self.run_pass(b, first)
         torch.cuda.synchronize()
         t0 = torch.cuda.Event(enable_timing=True)
         t1 = torch.cuda.Event(enable_timing=True)
         t0.record(self.stream)
         tok = 0
-        for _ in range(steps):
-            tok += self.step(n)
+        for _ in range(reps):
+            tok += self.run_pass(b, first)
         t1.record(self.stream)
         torch.cuda.synchronize()
-        ms = t0.elapsed_time(t1)
-        return ms / steps, tok / steps
+        return t0.elapsed_time(t1) / reps, tok / reps
 
-    def profile_steps(self, n, steps):
+    def profile_passes(self, b, reps, first=None):
         import torch
         self.enc.profile_read()
         self.enc.profile_enable(True)
-        for _ in range(steps):
-            self.step(n)
+        for _ in range(reps):
+            self.run_pass(b, first)
         torch.cuda.synchronize()
         self.enc.profile_enable(False)
         return self.enc.profile_read()
+
+    def close(self):
+        import torch
+        torch.cuda.synchronize()
+        self.enc.close()
+        del self.items, self.wdev, self.out
+        torch.cuda.empty_cache()
 
 
 def mfma_fraction(prof):
@@ -144,14 +174,54 @@ def mfma_fraction(prof):
     return (fl / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS) if ms > 0 else None
 
 
-def cpu_baseline(preset, wl, budget_s):
-    import numpy as np
+def sweep_rows(wl, sizes, reps, profile):
+    """Throughput of one pass over the pool at each micro-batch size."""
+    rows = []
+    for b in sizes:
+        ms, tok = wl.time_passes(b, reps, 1)
+        row = {"micro_batch": b, "tokens_per_s": tok / (ms * 1e-3), "items_per_s": wl.pool / (ms * 1e-3),
+               "ms_per_pass": ms, "micro_batches_per_pass": -(-wl.pool // b)}
+        if profile:
+            prof = wl.profile_passes(b, 1)
+            fl = sum(v["flops"] for v in prof.values())
+            row["gemm_attn_mfma_frac"] = mfma_fraction(prof)
+            row["whole_call_mfma_frac"] = fl / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS
+            if b == max(sizes):
+                row["kernels"] = kernel_table(prof, 1)
+        rows.append(row)
+    return rows
+
+
+def kernel_table(prof, passes):
+    """Per-kernel time per pass, share, and TFLOP/s (MFMA kernels) or GB/s."""
+    total_ms = sum(v["ms"] for v in prof.values())
+    return {k: {"ms_per_step": v["ms"] / passes, "share": v["ms"] / total_ms,
+                "tflops" if k.startswith(MFMA_KERNELS) else "gbs":
+                    (v["flops"] / (v["ms"] * 1e-3) / 1e12) if k.startswith(MFMA_KERNELS)
+                    else (v["bytes"] / (v["ms"] * 1e-3) / 1e9)}
+            for k, v in sorted(prof.items(), key=lambda kv: -kv[1]["ms"])}
+
+
+def oracle_threads():
     from threadpoolctl import threadpool_info
+    return max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def cpu_baseline(preset, wl, batch, budget_s):
     from oracle import encoder as O
-    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
     t0 = time.time()
     n_items, tokens = 0, 0
-    while n_items < wl.batch:
+    while n_items < batch:
         item = wl.items_host[n_items]
         packed, cu, grid = O.pack(preset, [item])
         O.encode(preset, wl.weights_host, packed, cu, grid)
@@ -160,10 +230,50 @@ def cpu_baseline(preset, wl, budget_s):
         if time.time() - t0 >= budget_s:
             break
     dt = time.time() - t0
-    return {"value": tokens / dt, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+    return {"value": tokens / dt, "unit": "tokens/s", "cores": oracle_threads(), "kind": "oracle",
             "sample": "%d of the %d requests, full %d-layer depth, float64, one request per call "
-                      "(%.1f s)" % (n_items, wl.batch, preset["layers"], dt),
-            "items_per_s": n_items / dt}
+                      "(%.1f s)" % (n_items, batch, preset["layers"], dt),
+            "items_per_s": n_items / dt, "cpu_model": cpu_model()}
+
+
+def cpu_config_timing(preset, wl, budget_s):
+    """The reference on the pool's first request (micro-batch 1).  Full depth
+    when a one-layer run says it fits the budget; otherwise one- and two-layer
+    runs, whose difference gives the per-layer time, and a full-depth
+    estimate from them."""
+    from paper_2609_31551_amd import configs as C
+    from oracle import encoder as O
+    packed, cu, grid = O.pack(preset, [wl.items_host[0]])
+    tokens = int(cu[-1])
+
+    def run(layers):
+        t0 = time.time()
+        O.encode(C.with_layers(preset, layers), wl.weights_host, packed, cu, grid)
+        return time.time() - t0
+
+    t1 = run(1)
+    rec = {"micro_batch": 1, "tokens": tokens, "cores": oracle_threads()}
+    if t1 * preset["layers"] <= budget_s:
+        tf = run(preset["layers"]) if preset["layers"] > 1 else t1
+        rec.update(depth=preset["layers"], seconds=tf, tokens_per_s=tokens / tf, measured_full_depth=True)
+        return rec
+    t2 = run(2)
+    per_layer = max(t2 - t1, 1e-9)
+    est = (t1 - per_layer) + preset["layers"] * per_layer
+    rec.update(depth=2, seconds=t2, tokens_per_s_at_depth=tokens / t2, per_layer_s=per_layer,
+               full_depth_estimate_s=est, tokens_per_s=tokens / est, measured_full_depth=False)
+    return rec
+
+
+def parse_workloads(spec):
+    out = []
+    for part in spec.split(";"):
+        part = part.strip()
+        if not part:
+            continue
+        name, pool, sizes = part.split(":")
+        out.append((name, int(pool), [int(b) for b in sizes.split(",") if b.strip()]))
+    return out
 
 
 def main():
@@ -180,10 +290,10 @@ def main():
     preset = C.PRESETS[args.preset]
     torch.cuda.set_device(0)
     sweep = [int(b) for b in args.sweep.split(",") if b.strip()]
-    wl = Workload(preset, max([args.batch] + sweep))
+    pool = max([args.batch] + sweep)
+    wl = Workload(preset, pool, pool)
 
-    ms, tok = wl.time_steps(args.batch, args.steps, args.warmup)
-    items_per_s = args.batch / (ms * 1e-3)
+    ms, tok = wl.time_passes(args.batch, args.steps, args.warmup, first=args.batch)
     result = {
         "metric": METRIC, "value": tok / (ms * 1e-3), "unit": "tokens/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True,
@@ -192,10 +302,10 @@ def main():
                                % (preset["name"], args.batch, tok),
                    "micro_batch": args.batch, "tokens_per_step": tok, "layers": preset["layers"],
                    "hidden": preset["hidden"], "parallelism": "single GPU"},
-        "images_per_s": items_per_s,
+        "images_per_s": args.batch / (ms * 1e-3),
     }
     if not args.no_profile:
-        prof = wl.profile_steps(args.batch, args.steps)
+        prof = wl.profile_passes(args.batch, args.steps, first=args.batch)
         dom = max(prof, key=lambda k: prof[k]["ms"])
         p = prof[dom]
         is_mfma = dom.startswith(MFMA_KERNELS)
@@ -210,25 +320,30 @@ def main():
                               "peak": peak, "unit": unit, "frac": achieved / peak,
                               "traffic": traffic_record(dom), "mean_launch_ms": per_launch_ms,
                               "launches_per_step": p["launches"] / args.steps}
-        total_ms = sum(v["ms"] for v in prof.values())
-        result["kernels"] = {k: {"ms_per_step": v["ms"] / args.steps, "share": v["ms"] / total_ms,
-                                 "tflops" if k.startswith(MFMA_KERNELS) else "gbs":
-                                     (v["flops"] / (v["ms"] * 1e-3) / 1e12) if k.startswith(MFMA_KERNELS)
-                                     else (v["bytes"] / (v["ms"] * 1e-3) / 1e9)}
-                             for k, v in sorted(prof.items(), key=lambda kv: -kv[1]["ms"])}
+        result["kernels"] = kernel_table(prof, args.steps)
         result["gemm_attn_mfma_frac"] = mfma_fraction(prof)
+    workloads = {}
     if sweep:
-        rows = []
-        for b in sweep:
-            ms_b, tok_b = wl.time_steps(b, args.sweep_steps, 2)
-            row = {"micro_batch": b, "tokens_per_s": tok_b / (ms_b * 1e-3), "items_per_s": b / (ms_b * 1e-3),
-                   "ms_per_step": ms_b}
-            if not args.no_profile:
-                row["gemm_attn_mfma_frac"] = mfma_fraction(wl.profile_steps(b, args.sweep_steps))
-            rows.append(row)
-        result["sweep"] = rows
+        workloads[preset["name"]] = {"pool": pool, "sweep": sweep_rows(wl, sweep, args.sweep_steps,
+                                                                       not args.no_profile)}
+    cpu_configs = {}
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(preset, wl, args.cpu_budget_s)
+        result["cpu_baseline"] = cpu_baseline(preset, wl, args.batch, args.cpu_budget_s)
+        if args.cpu_configs_budget_s > 0:
+            cpu_configs[preset["name"]] = cpu_config_timing(preset, wl, args.cpu_configs_budget_s)
+    wl.close()
+    for name, wpool, sizes in parse_workloads(args.workloads):
+        other = Workload(C.PRESETS[name], wpool, max(sizes))
+        workloads[name] = {"pool": wpool, "pool_tokens": sum(other.item_tokens),
+                           "sweep": sweep_rows(other, sizes, args.sweep_steps, not args.no_profile)}
+        if not args.no_cpu_baseline and args.cpu_configs_budget_s > 0:
+            cpu_configs[name] = cpu_config_timing(C.PRESETS[name], other, args.cpu_configs_budget_s)
+        other.close()
+        print("[bench] %s swept" % name, file=sys.stderr, flush=True)
+    if workloads:
+        result["workloads"] = workloads
+    if cpu_configs:
+        result["cpu_configs"] = cpu_configs
     print(json.dumps(result), flush=True)
 
 
