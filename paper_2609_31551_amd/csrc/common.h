@@ -75,6 +75,14 @@ struct GemmArgs {
 
 // ---- launchers (each returns hipGetLastError() of its launch) --------------
 hipError_t launch_gemm_bf16(const GemmArgs& a, hipStream_t s, const char** kname);
+// Rows [0, h) of a bf16 GEMM whose last round of 256 x 256 tiles would run
+// mostly empty: launched as whole rounds, rows [h, M) as a second launch with
+// a smaller tile.  0 when one launch is as fast.
+int gemm_bf16_head_rows(const GemmArgs& a);
+// The same GEMM restricted to output rows [m0, m1) (pointers and row-indexed
+// epilogue streams shifted; a period-indexed position table needs
+// m0 % pos_period == 0).
+GemmArgs gemm_rows(const GemmArgs& a, int m0, int m1);
 hipError_t launch_gemm_bf16_staged(const GemmArgs& a, hipStream_t s, const char** kname);
 hipError_t launch_gemm_f32(const GemmArgs& a, hipStream_t s, const char** kname);
 

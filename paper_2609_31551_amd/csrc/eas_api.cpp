@@ -288,7 +288,20 @@ GemmArgs gemm_args(int M, int N, int K, const void* A, int lda, const void* B, i
   return g;
 }
 
+eas_status gemm_launch(eas_encoder* e, const GemmArgs& g, hipStream_t s);
+
 eas_status gemm(eas_encoder* e, const GemmArgs& g, hipStream_t s) {
+  if (e->cfg.dtype == EAS_BF16) {
+    const int h = gemm_bf16_head_rows(g);
+    if (h > 0) {
+      const eas_status rc = gemm_launch(e, gemm_rows(g, 0, h), s);
+      return rc != EAS_OK ? rc : gemm_launch(e, gemm_rows(g, h, g.M), s);
+    }
+  }
+  return gemm_launch(e, g, s);
+}
+
+eas_status gemm_launch(eas_encoder* e, const GemmArgs& g, hipStream_t s) {
   const bool bf = e->cfg.dtype == EAS_BF16;
   const double el = bf ? 2.0 : 4.0;
   const double flops = 2.0 * g.M * g.N * (double)g.K;

@@ -18,11 +18,13 @@
 //  * v_mfma_f32_32x32x16_bf16, each wave a (BM/WGM) x (BN/WGN) sub-tile of
 //    32 x 32 blocks (8 waves of 64 x 128 for the 256 x 256 tile); operand
 //    fragments for the next 16-wide k slice are read while the current
-//    slice's MFMAs run, and the barrier sits before the last slice so its
-//    wait overlaps queued MFMAs.
+//    slice's MFMAs run (the issue order is pinned: one read between two
+//    MFMAs), and the barrier sits before the last slice so its wait overlaps
+//    queued MFMAs.
 //  * Tiles are handed out XCD-aware: workgroups are dispatched round-robin
 //    over the 8 XCDs, so block b is remapped to give every XCD a contiguous
-//    run of output tiles that share A row panels in that XCD's L2.
+//    run of output tiles, ordered in groups of 4 tile rows swept column by
+//    column, so the tiles an XCD runs together share operand panels in its L2.
 //  * Fused epilogue through LDS: each wave stages 32 rows of its fp32
 //    accumulators, then every lane owns 8 consecutive columns of a row and
 //    applies bias, GELU / QuickGELU, a position-table row and the fp32
@@ -76,6 +78,17 @@ __device__ __forceinline__ int xcd_tile(int b, int nb) {
   return (x < full ? x * per : full * per + (x - full) * (per - 1)) + s;
 }
 
+// Linear tile index -> (tile row, tile column), in groups of GROUP_M tile rows
+// swept column by column, so the ~32 tiles an XCD runs at once form a
+// GROUP_M x 8 block and share fewer operand panels in its L2.
+constexpr int GROUP_M = 4;
+__device__ __forceinline__ void tile_coords(int t, int mt, int nt, int& mi, int& ni) {
+  const int g = t / (GROUP_M * nt), r = t % (GROUP_M * nt);
+  const int rows = min(GROUP_M, mt - g * GROUP_M);
+  ni = r / rows;
+  mi = g * GROUP_M + r % rows;
+}
+
 template <int BM, int BN, int WGM, int WGN>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_tile_kernel(GemmArgs a) {
   using C = Cfg<BM, BN, WGM, WGN>;
@@ -85,8 +98,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_tile_kernel(GemmArgs
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WGN, wn = wave % WGN;
   const int tiles_n = (a.N + BN - 1) / BN;
-  const int bid = xcd_tile(blockIdx.x, gridDim.x);
-  const int m0 = (bid / tiles_n) * BM, n0 = (bid % tiles_n) * BN;
+  int mi, ni;
+  tile_coords(xcd_tile(blockIdx.x, gridDim.x), (a.M + BM - 1) / BM, tiles_n, mi, ni);
+  const int m0 = mi * BM, n0 = ni * BN;
   const int KT = a.K / BK;
   const bf16* A = static_cast<const bf16*>(a.A);
   const bf16* B = static_cast<const bf16*>(a.B);
@@ -152,6 +166,19 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_tile_kernel(GemmArgs
       for (int j = 0; j < C::FN; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
   };
+  // pin the issue order of one slice: each fragment read of the next slice
+  // goes between two MFMAs of this one, so LDS latency hides under the MFMAs
+  auto interleave = [&]() {
+    constexpr int NR = C::FM + C::FN, NM = C::FM * C::FN;
+    static_assert(NM >= NR, "more reads than MFMAs per slice");
+#pragma unroll
+    for (int i = 0; i < NR; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one LDS read
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, NM - NR, 0);
+    __builtin_amdgcn_sched_barrier(0);
+  };
 
   // prologue: tiles 0 .. ST-1 in flight; wait for tile 0
 #pragma unroll
@@ -162,22 +189,35 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_tile_kernel(GemmArgs
   __syncthreads();
   load_frags(0, cofs[0], fa[0], fb[0]);
 
-  for (int kt = 0; kt < KT; ++kt) {
+  // every k-tile but the last; the loop body has no branch around its MFMAs,
+  // so the next tile's first fragment reads interleave with this tile's last slice
+  for (int kt = 0; kt < KT - 1; ++kt) {
     const int st = kt % ST;
 #pragma unroll
     for (int h = 0; h < NH - 1; ++h) {
       load_frags(st, cofs[h + 1], fa[(h + 1) & 1], fb[(h + 1) & 1]);
       mma(fa[h & 1], fb[h & 1]);
+      interleave();
     }
-    if (kt + 1 < KT) {
-      // this wave's reads of stage st are done once lgkmcnt drains; tile kt+1
-      // (the newest DMA) has landed at vmcnt 0; after the barrier every wave
-      // is past stage st, which is refilled with tile kt+ST
-      wait_lds();
-      wait_vm<0>();
-      __builtin_amdgcn_s_barrier();
-      if (kt + ST < KT) issue(kt + ST, st);
-      load_frags((kt + 1) % ST, cofs[0], fa[NH & 1], fb[NH & 1]);
+    // this wave's reads of stage st are done once lgkmcnt drains; tile kt+1
+    // (the newest DMA) has landed at vmcnt 0; after the barrier every wave
+    // is past stage st, which is refilled with tile kt+ST
+    wait_lds();
+    wait_vm<0>();
+    __builtin_amdgcn_s_barrier();
+    if (kt + ST < KT) issue(kt + ST, st);
+    __builtin_amdgcn_sched_barrier(0);
+    load_frags((kt + 1) % ST, cofs[0], fa[NH & 1], fb[NH & 1]);
+    mma(fa[(NH - 1) & 1], fb[(NH - 1) & 1]);
+    interleave();
+  }
+  {
+    const int st = (KT - 1) % ST;
+#pragma unroll
+    for (int h = 0; h < NH - 1; ++h) {
+      load_frags(st, cofs[h + 1], fa[(h + 1) & 1], fb[(h + 1) & 1]);
+      mma(fa[h & 1], fb[h & 1]);
+      interleave();
     }
     mma(fa[(NH - 1) & 1], fb[(NH - 1) & 1]);
   }
@@ -294,27 +334,72 @@ bool tile_ok(const GemmArgs& a) {
 
 }  // namespace
 
-hipError_t launch_gemm_bf16(const GemmArgs& a, hipStream_t s, const char** kname) {
-  if (!tile_ok(a)) return launch_gemm_bf16_staged(a, s, kname);
-  // Pick the tile by estimated time: full-chip rounds (256 CUs; one 256-wide
-  // or two 128 x 128 workgroups per CU) times the tile's work over its
-  // measured relative efficiency.  All tiles sum k in the same order, so the
-  // choice never changes a result.
-  struct Opt { int bm, bn, per_cu; double eff; };
-  const Opt opts[3] = {{256, 256, 1, 1.00}, {256, 128, 1, 0.80}, {128, 128, 2, 0.65}};
+namespace {
+
+// Tile options, fitted to measured launch times on the encoder's shapes.
+// `slots` workgroups fit on the chip at once (two 128 x 128 workgroups share
+// a CU); a round of them costs area * slots / 256 / eff in units where a
+// full round of 256 x 256 tiles costs 65536.  A 128 x 128 launch of at most
+// 256 tiles runs one workgroup per CU, at about 0.7 of a shared round.
+struct TileOpt { int bm, bn, slots; double eff; };
+constexpr TileOpt kTiles[3] = {{256, 256, 256, 1.00}, {256, 128, 256, 0.80}, {128, 128, 512, 0.90}};
+
+double tile_time(const TileOpt& o, long M, long N) {
+  const long tiles = ((M + o.bm - 1) / o.bm) * ((N + o.bn - 1) / o.bn);
+  const double round = (double)o.bm * o.bn * (o.slots / 256) / o.eff;
+  if (o.slots > 256 && tiles <= 256) return 0.7 * round;
+  return (double)((tiles + o.slots - 1) / o.slots) * round;
+}
+
+int best_tile(long M, long N, double* t) {
   int best = 0;
   double best_t = 1e300;
   for (int i = 0; i < 3; ++i) {
-    const long tiles = (long)((a.M + opts[i].bm - 1) / opts[i].bm) * ((a.N + opts[i].bn - 1) / opts[i].bn);
-    const long slots = 256L * opts[i].per_cu;
-    const double t = (double)((tiles + slots - 1) / slots) * opts[i].bm * opts[i].bn * opts[i].per_cu / opts[i].eff;
-    if (t < best_t) { best_t = t; best = i; }
+    const double ti = tile_time(kTiles[i], M, N);
+    if (ti < best_t) { best_t = ti; best = i; }
   }
-  switch (best) {
+  if (t) *t = best_t;
+  return best;
+}
+
+}  // namespace
+
+hipError_t launch_gemm_bf16(const GemmArgs& a, hipStream_t s, const char** kname) {
+  if (!tile_ok(a)) return launch_gemm_bf16_staged(a, s, kname);
+  // Pick the tile by estimated time.  All tiles sum k in the same order, so
+  // the choice never changes a result.
+  switch (best_tile(a.M, a.N, nullptr)) {
     case 0: *kname = "gemm_bf16_256x256"; return launch_tile<256, 256, 4, 2>(a, s);
     case 1: *kname = "gemm_bf16_256x128"; return launch_tile<256, 128, 4, 2>(a, s);
     default: *kname = "gemm_bf16_128x128"; return launch_tile<128, 128, 2, 2>(a, s);
   }
+}
+
+int gemm_bf16_head_rows(const GemmArgs& a) {
+  if (!tile_ok(a)) return 0;
+  const long nt = (a.N + 255) / 256, tiles = (long)((a.M + 255) / 256) * nt;
+  const long rounds = tiles / 256;
+  if (rounds == 0 || tiles % 256 == 0) return 0;
+  const long head = rounds * 256 / nt * 256;   // rows covered by whole rounds of 256 x 256 tiles
+  if (head <= 0 || head >= a.M) return 0;
+  if (a.pos && !a.pos_idx && head % a.pos_period) return 0;
+  double whole, tail;
+  best_tile(a.M, a.N, &whole);
+  best_tile(a.M - head, a.N, &tail);
+  const double split = tile_time(kTiles[0], head, a.N) + tail;
+  return split < 0.97 * whole ? (int)head : 0;
+}
+
+GemmArgs gemm_rows(const GemmArgs& a, int m0, int m1) {
+  GemmArgs r = a;
+  r.M = m1 - m0;
+  const size_t ea = a.stats ? 4 : 2;   // fp32 rows when the LayerNorm is applied on the fly
+  r.A = static_cast<const char*>(a.A) + (size_t)m0 * a.lda * ea;
+  if (a.stats) r.stats = a.stats + (size_t)m0 * a.ln_group;
+  r.out = static_cast<char*>(a.out) + (size_t)m0 * a.ldo * (a.out_f32 ? 4 : 2);
+  if (a.resid) r.resid = a.resid + (size_t)m0 * a.ldr;
+  if (a.pos_idx) r.pos_idx = a.pos_idx + m0;
+  return r;
 }
 
 }  // namespace eas
