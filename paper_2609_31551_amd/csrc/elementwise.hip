@@ -93,6 +93,55 @@ __global__ __launch_bounds__(256) void ln_apply_kernel(const float* x, int N, in
   }
 }
 
+// Vector form: one wave per row, each lane 4 consecutive elements per 16-byte
+// chunk (rows with d % 4 == 0, up to 64 * 4 * LNV_MAXC wide).
+constexpr int LNV_MAXC = 8;
+
+template <class W, class Y>
+__global__ __launch_bounds__(256) void ln_apply_vec_kernel(const float* x, int N, int d, float eps, const W* g,
+                                                           const W* b, Y* y) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= N) return;
+  const int lane = threadIdx.x & 63, nc = d >> 2;
+  const float4* xr = reinterpret_cast<const float4*>(x + (long)row * d);
+  float4 v[LNV_MAXC];
+  float s = 0.0f;
+#pragma unroll
+  for (int e = 0; e < LNV_MAXC; ++e) {
+    const int c = lane + 64 * e;
+    v[e] = c < nc ? xr[c] : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    s += (v[e].x + v[e].y) + (v[e].z + v[e].w);
+  }
+  const float mean = wave_sum(s) / (float)d;
+  float q = 0.0f;
+#pragma unroll
+  for (int e = 0; e < LNV_MAXC; ++e) {
+    if (lane + 64 * e < nc) {
+      const float a0 = v[e].x - mean, a1 = v[e].y - mean, a2 = v[e].z - mean, a3 = v[e].w - mean;
+      q += (a0 * a0 + a1 * a1) + (a2 * a2 + a3 * a3);
+    }
+  }
+  const float rstd = 1.0f / sqrtf(wave_sum(q) / (float)d + eps);
+#pragma unroll
+  for (int e = 0; e < LNV_MAXC; ++e) {
+    const int c = lane + 64 * e;
+    if (c < nc) {
+      const float in[4] = {v[e].x, v[e].y, v[e].z, v[e].w};
+      Y out[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) out[j] = (Y)((in[j] - mean) * rstd * (float)g[4 * c + j] + (float)b[4 * c + j]);
+      if constexpr (sizeof(Y) == 2) {
+        union { uint2 u; Y h[4]; } o;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) o.h[j] = out[j];
+        *reinterpret_cast<uint2*>(y + (long)row * d + 4 * c) = o.u;
+      } else {
+        *reinterpret_cast<float4*>(y + (long)row * d + 4 * c) = make_float4(out[0], out[1], out[2], out[3]);
+      }
+    }
+  }
+}
+
 // Rotate the pairs (k, k + hd/2) of every head of q and k in place; slot k
 // turns by pos[axis(k)] * inv_freq[k].
 template <class T>
@@ -117,6 +166,43 @@ __global__ void rope_kernel(T* qkv, int ldqkv, int N, int heads, int hd, const i
     const float x1 = (float)base[k], x2 = (float)base[k + half];
     base[k] = (T)(x1 * cs - x2 * sn);
     base[k + half] = (T)(x2 * cs + x1 * sn);
+  }
+}
+
+// bf16 form: one thread per (token, 8 consecutive slots); the 8 angles are
+// computed once and applied to every head of q and of k with 16-byte
+// accesses (hd % 16 == 0).
+__global__ void rope_vec_kernel(bf16* qkv, int ldqkv, int N, int heads, int hd, const int4* pos3,
+                                const float* inv_freq, const int* slot_axis) {
+  const int half = hd >> 1, chunks = half >> 3;
+  const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (long)N * chunks) return;
+  const int i = (int)(idx / chunks), k0 = (int)(idx % chunks) * 8;
+  const int4 p = pos3[i];
+  float sn[8], cs[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int ax = slot_axis[k0 + j];
+    const float pos = (float)(ax == 0 ? p.x : (ax == 1 ? p.y : p.z));
+    sincosf(pos * inv_freq[k0 + j], &sn[j], &cs[j]);
+  }
+  const int dq = heads * hd;
+  for (int part = 0; part < 2; ++part) {   // q block, then k block
+    for (int h = 0; h < heads; ++h) {
+      bf16* base = qkv + (long)i * ldqkv + part * dq + h * hd + k0;
+      union { uint4 u; bf16 e[8]; } a, c;
+      a.u = *reinterpret_cast<const uint4*>(base);
+      c.u = *reinterpret_cast<const uint4*>(base + half);
+      union { uint4 u; bf16 e[8]; } oa, oc;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float x1 = (float)a.e[j], x2 = (float)c.e[j];
+        oa.e[j] = (bf16)(x1 * cs[j] - x2 * sn[j]);
+        oc.e[j] = (bf16)(x2 * cs[j] + x1 * sn[j]);
+      }
+      *reinterpret_cast<uint4*>(base) = oa.u;
+      *reinterpret_cast<uint4*>(base + half) = oc.u;
+    }
   }
 }
 
@@ -196,6 +282,17 @@ hipError_t launch_ln_apply(const float* x, int N, int d, float eps, const void* 
                            void* y, int y_f32, hipStream_t s) {
   if (d > 64 * LN_MAXE) return hipErrorInvalidValue;
   const dim3 grid(blocks_for(N, 4)), blk(256);
+  const bool al = (uintptr_t)x % 16 == 0 && (uintptr_t)y % (y_f32 ? 16 : 8) == 0 &&
+                  (uintptr_t)g % (w_bf16 ? 8 : 16) == 0 && (uintptr_t)b % (w_bf16 ? 8 : 16) == 0;
+  if (d % 4 == 0 && d <= 256 * LNV_MAXC && al && w_bf16) {
+    if (y_f32)
+      hipLaunchKernelGGL((ln_apply_vec_kernel<bf16, float>), grid, blk, 0, s, x, N, d, eps, (const bf16*)g,
+                         (const bf16*)b, (float*)y);
+    else
+      hipLaunchKernelGGL((ln_apply_vec_kernel<bf16, bf16>), grid, blk, 0, s, x, N, d, eps, (const bf16*)g,
+                         (const bf16*)b, (bf16*)y);
+    return hipGetLastError();
+  }
   if (w_bf16 && y_f32)
     hipLaunchKernelGGL((ln_apply_kernel<bf16, float>), grid, blk, 0, s, x, N, d, eps, (const bf16*)g, (const bf16*)b, (float*)y);
   else if (w_bf16)
@@ -210,6 +307,12 @@ hipError_t launch_ln_apply(const float* x, int N, int d, float eps, const void* 
 hipError_t launch_rope(void* qkv, int ldqkv, int N, int heads, int hd, int is_bf16, const int4* pos3,
                        const float* inv_freq, const int* slot_axis, hipStream_t s) {
   const long total = (long)N * heads * (hd / 2);
+  if (is_bf16 && hd % 16 == 0 && ldqkv % 8 == 0 && (uintptr_t)qkv % 16 == 0) {
+    const long threads = (long)N * (hd / 16);
+    hipLaunchKernelGGL(rope_vec_kernel, dim3(blocks_for(threads, 256)), dim3(256), 0, s, (bf16*)qkv, ldqkv, N, heads,
+                       hd, pos3, inv_freq, slot_axis);
+    return hipGetLastError();
+  }
   if (is_bf16)
     hipLaunchKernelGGL((rope_kernel<bf16>), dim3(blocks_for(total, 256)), dim3(256), 0, s, (bf16*)qkv, ldqkv, N,
                        heads, hd, pos3, inv_freq, slot_axis);
