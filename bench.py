@@ -318,7 +318,8 @@ def main():
             peak, unit = PEAK_HBM_GBS, "GB/s"
         result["roofline"] = {"bound": "mfma" if is_mfma else "hbm", "kernel": dom, "achieved": achieved,
                               "peak": peak, "unit": unit, "frac": achieved / peak,
-                              "traffic": traffic_record(dom), "mean_launch_ms": per_launch_ms,
+                              "traffic": traffic_record(dom), "traffic_unit": "HBM bytes per launch",
+                              "mean_launch_ms": per_launch_ms,
                               "launches_per_step": p["launches"] / args.steps}
         result["kernels"] = kernel_table(prof, args.steps)
         result["gemm_attn_mfma_frac"] = mfma_fraction(prof)
