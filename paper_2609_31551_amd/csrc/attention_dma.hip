@@ -14,7 +14,9 @@
 //    past its end re-read the last row and are masked out of the softmax.
 //  * Both tiles are stored row-major with a per-row rotation of the 16-byte
 //    chunks (2(r&3) + ((r>>2)&1) for 8-chunk rows, (r>>2)&1 for 10-chunk
-//    rows) that keeps both access patterns below free of bank conflicts.
+//    rows), which keeps the transposing V reads free of bank conflicts; the
+//    K reads see at most 2-way conflicts (a conflict-free K order measured
+//    no faster).
 //  * S^T = K Q^T (K rows as the A operand, Q in registers as the B operand):
 //    lane l holds 16 scores of query l % 32, so the online softmax is
 //    lane-local except one cross-half shuffle for the running max.
@@ -49,6 +51,7 @@ struct AttnCfg {
   static constexpr int BUF = 2 * TILE;             // K + V
   static constexpr int DMA = R / 2;                // DMA instructions per wave per operand per tile
   __device__ static int rot(int row) { return R == 8 ? 2 * (row & 3) + ((row >> 2) & 1) : ((row >> 2) & 1); }
+  // logical chunk L of row `row` sits at physical chunk phys(row, L)
   __device__ static int phys(int row, int L) { return (L + rot(row)) % R; }
   __device__ static int logical(int row, int p) { return (p + R - rot(row)) % R; }
 };
@@ -92,10 +95,9 @@ __global__ __launch_bounds__(128) void attn_bf16_dma_kernel(AttnArgs a, AttnWork
     const unsigned base = lds0 + buf * C::BUF;
 #pragma unroll
     for (int j = 0; j < C::DMA; ++j) {
-      const int key = min(k0 + drow[j], s1 - 1);
-      const unsigned off = (unsigned)(((long)key * a.ldqkv + dcol[j]) * 2);
-      dma16(base + (wave * C::DMA + j) * 1024, off + dq * 2, qkv);               // K
-      dma16(base + C::TILE + (wave * C::DMA + j) * 1024, off + 2 * dq * 2, qkv); // V
+      const long key = min(k0 + drow[j], s1 - 1);
+      dma16(base + (wave * C::DMA + j) * 1024, (unsigned)((key * a.ldqkv + dq + dcol[j]) * 2), qkv);
+      dma16(base + C::TILE + (wave * C::DMA + j) * 1024, (unsigned)((key * a.ldqkv + 2 * dq + dcol[j]) * 2), qkv);
     }
   };
 
@@ -189,7 +191,10 @@ __global__ __launch_bounds__(128) void attn_bf16_dma_kernel(AttnArgs a, AttnWork
         float mx = sc[qb][0];
 #pragma unroll
         for (int e = 1; e < 16; ++e) mx = fmaxf(mx, sc[qb][e]);
-        mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * c;
+        {   // both 16-key halves of query l % 32: lanes l and l ^ 32, swapped in VALU
+          const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+          mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1])) * c;
+        }
         const bool need = mx > m_run[qb] + 8.0f;
         if (__any(need)) {
           const float m_new = need ? fmaxf(m_run[qb], mx) : m_run[qb];

@@ -1,0 +1,77 @@
+"""GPU parity at the benchmarked sizes, in the launch configurations the
+benchmark times.
+
+Each test encodes a whole benchmarked micro-batch (the same seeded request
+pools as bench.py) and checks sampled requests against the fp64 reference run
+on that request alone, at full depth where the reference finishes in seconds
+and at two layers otherwise; it also checks that each sampled request's rows
+are bit-identical to its own micro-batch-1 encoding.  At these sizes the
+GEMMs run the large-tile path, including the split of quantised grids into a
+256 x 256 head launch and a 128 x 128 tail launch, and attention runs over the
+longest sequences (9216-token images, 8192-token clips).
+"""
+import numpy as np
+import pytest
+
+from _harness import TOL, gpu_encode, oracle_encode, rel_err
+from paper_2609_31551_amd import configs as C
+from paper_2609_31551_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+
+def _check_samples(p, items, W, samples, max_tokens=None):
+    batch = gpu_encode(p, items, W, max_tokens=max_tokens)
+    cu = batch["cu_out"]
+    for r in samples:
+        print("[full-size] %s: request %d of %d" % (p["name"], r, len(items)), flush=True)
+        ref = oracle_encode(p, [items[r]], W)
+        e = rel_err(batch["out"][cu[r]:cu[r + 1]], ref["out"])
+        print("[full-size] %s: request %d relative error %.3g" % (p["name"], r, e), flush=True)
+        assert e <= TOL[p["dtype"]], (r, e)
+        alone = gpu_encode(p, [items[r]], W, enc=batch["enc"], wdev=batch["wdev"])
+        np.testing.assert_array_equal(alone["out"], batch["out"][cu[r]:cu[r + 1]])
+
+
+def test_clip_microbatch_64_full_depth():
+    """The headline workload: 64 CLIP images (36928 tokens), full depth;
+    request 63 sits in the rows of the tail launches of the split GEMMs."""
+    p = C.CLIP_L336
+    W = synth.make_weights(p, 0)
+    items = synth.make_items(p, 64, 0)
+    _check_samples(p, items, W, [5, 63])
+
+
+def test_qwen_image_microbatch_8_full_depth():
+    """The first 8 images of the 64-image pool (variable resolution), full
+    depth; the smallest image is checked against the reference."""
+    p = C.QWEN_IMAGE
+    W = synth.make_weights(p, 0)
+    items = synth.make_items(p, 64, 0)[:8]
+    sizes = [a.shape[2] * a.shape[3] for a in items]
+    _check_samples(p, items, W, [int(np.argmin(sizes))])
+
+
+def test_qwen_image_largest_images_two_layers():
+    """Micro-batch with 1344 x 1344 images (9216 tokens each, the longest
+    attention rows of the image workload) at two layers."""
+    p = C.with_layers(C.QWEN_IMAGE, 2)
+    W = synth.make_weights(p, 0)
+    items = synth.make_items(p, 3, 0, shapes=[(2, 1344, 1344), (2, 672, 1344), (2, 1344, 1344)])
+    _check_samples(p, items, W, [2])
+
+
+def test_video_microbatch_4_two_layers():
+    """4 clips of 16 x 448 x 448 (32768 tokens, 8192 per clip), two layers."""
+    p = C.with_layers(C.QWEN_VIDEO, 2)
+    W = synth.make_weights(p, 0)
+    items = synth.make_items(p, 4, 0)
+    _check_samples(p, items, W, [3])
+
+
+def test_whisper_microbatch_32_full_depth():
+    """32 audio clips (48000 tokens), full depth."""
+    p = C.WHISPER_L
+    W = synth.make_weights(p, 0)
+    items = synth.make_items(p, 32, 0)
+    _check_samples(p, items, W, [31])
