@@ -24,6 +24,9 @@
 //    operand layout; the V^T operand comes straight from the row-major V
 //    tile through ds_read_b64_tr_b16, whose 16-lane transpose turns four
 //    8-byte row pieces into four columns.
+//  * For head_dim 64, both halves' S^T MFMAs of a 64-key tile are issued
+//    before the first softmax, so the softmax of one half overlaps MFMAs of
+//    the other (head_dim 80 has no registers for the second score block).
 //  * A 32-key half tile that lies wholly past the sequence end is skipped,
 //    and a wave whose queries all lie past the end skips the arithmetic.
 #include "common.h"
@@ -50,6 +53,8 @@ struct AttnCfg {
   static constexpr int TILE = KTILE * R * 16;      // bytes of one K or V tile
   static constexpr int BUF = 2 * TILE;             // K + V
   static constexpr int DMA = R / 2;                // DMA instructions per wave per operand per tile
+  // issue both halves' S^T MFMAs ahead of the softmax (needs 2 more score blocks in VGPRs)
+  static constexpr bool OVERLAP = HD <= 64;
   __device__ static int rot(int row) { return R == 8 ? 2 * (row & 3) + ((row >> 2) & 1) : ((row >> 2) & 1); }
   // logical chunk L of row `row` sits at physical chunk phys(row, L)
   __device__ static int phys(int row, int L) { return (L + rot(row)) % R; }
@@ -155,12 +160,11 @@ __global__ __launch_bounds__(128) void attn_bf16_dma_kernel(AttnArgs a, AttnWork
     const char* Kt = smem + buf * C::BUF;
     const int nkb = k0 + 32 < s1 ? 2 : 1;   // 32-key halves holding at least one key
 
-    // the tile as two 32-key halves: S^T half -> softmax -> O^T update, so only
-    // one half's scores are live at a time
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      if (kb >= nkb) break;
-      f32x16 sc[2];
+    // Per 32-key half kb: S^T = K Q^T, online softmax, O^T += V^T P^T.  Both
+    // halves' S^T MFMAs are issued first, so the first half's softmax (VALU)
+    // runs while the second half's MFMAs execute, and the second half's
+    // softmax overlaps the first half's P V MFMAs.
+    auto scores = [&](int kb, f32x16* sc) {
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
@@ -172,11 +176,29 @@ __global__ __launch_bounds__(128) void attn_bf16_dma_kernel(AttnArgs a, AttnWork
         for (int qb = 0; qb < 2; ++qb)
           sc[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[qb][ks], sc[qb], 0, 0, 0);
       }
-      // Online softmax.  Scores are masked only in a half that reaches past the
-      // sequence end.  The running max m (log2 units, scale folded in) is raised
-      // lazily: O and the row sum keep a stale m until a lane's max exceeds it
-      // by more than 8, so p = 2^(s*c - m) <= 256 and the rescale of O is
-      // usually skipped; both share m, so O / sum is unchanged.
+    };
+    // V^T operand fragments of half kb: [ch][hb], 16 keys each
+    auto read_v = [&](int kb, bf16x8 (*va)[C::HB]) {
+#pragma unroll
+      for (int ch = 0; ch < 2; ++ch)
+#pragma unroll
+        for (int hb = 0; hb < C::HB; ++hb) {
+          union { bf16x8 v; v4i16 h[2]; } u;
+#pragma unroll
+          for (int half = 0; half < 2; ++half) {
+            const int rbase = (kb * 32 + 16 * ch + 8 * half) * C::R * 16;
+            u.h[half] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (lds_v4i16*)(lds + buf * C::BUF + C::TILE + rbase + vofs[hb]));
+          }
+          va[ch][hb] = u.v;
+        }
+    };
+    // Online softmax.  Scores are masked only in a half that reaches past the
+    // sequence end.  The running max m (log2 units, scale folded in) is raised
+    // lazily: O and the row sum keep a stale m until a lane's max exceeds it
+    // by more than 8, so p = 2^(s*c - m) <= 256 and the rescale of O is
+    // usually skipped; both share m, so O / sum is unchanged.
+    auto softmax = [&](int kb, f32x16* sc, bf16x8 (*pb)[2]) {
       const int kh = k0 + kb * 32;
       if (kh + 32 > s1) {
 #pragma unroll
@@ -185,7 +207,6 @@ __global__ __launch_bounds__(128) void attn_bf16_dma_kernel(AttnArgs a, AttnWork
           for (int e = 0; e < 16; ++e)
             if (kh + (e >> 2) * 8 + g * 4 + (e & 3) >= s1) sc[qb][e] = -INFINITY;
       }
-      bf16x8 pb[2][2];
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb) {
         float mx = sc[qb][0];
@@ -216,22 +237,42 @@ __global__ __launch_bounds__(128) void attn_bf16_dma_kernel(AttnArgs a, AttnWork
         }
         l_part[qb] += psum;
       }
-      // O^T += V^T P^T, 16 keys per MFMA
+    };
+    auto pv = [&](bf16x8 (*va)[C::HB], bf16x8 (*pb)[2]) {
 #pragma unroll
-      for (int ch = 0; ch < 2; ++ch) {
+      for (int ch = 0; ch < 2; ++ch)
 #pragma unroll
-        for (int hb = 0; hb < C::HB; ++hb) {
-          union { bf16x8 v; v4i16 h[2]; } va;
-#pragma unroll
-          for (int half = 0; half < 2; ++half) {
-            const int rbase = (kb * 32 + 16 * ch + 8 * half) * C::R * 16;
-            va.h[half] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                (lds_v4i16*)(lds + buf * C::BUF + C::TILE + rbase + vofs[hb]));
-          }
+        for (int hb = 0; hb < C::HB; ++hb)
 #pragma unroll
           for (int qb = 0; qb < 2; ++qb)
-            o[qb][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va.v, pb[qb][ch], o[qb][hb], 0, 0, 0);
-        }
+            o[qb][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[ch][hb], pb[qb][ch], o[qb][hb], 0, 0, 0);
+    };
+
+    bf16x8 va[2][C::HB], pa[2][2];
+    if constexpr (C::OVERLAP) {
+      f32x16 sa[2], sb[2];
+      scores(0, sa);
+      if (nkb == 2) scores(1, sb);
+      read_v(0, va);
+      __builtin_amdgcn_sched_barrier(0);
+      softmax(0, sa, pa);
+      pv(va, pa);
+      if (nkb == 2) {
+        __builtin_amdgcn_sched_barrier(0);
+        read_v(1, va);
+        softmax(1, sb, pa);
+        pv(va, pa);
+      }
+    } else {
+      // one half's scores live at a time (register budget of head_dim 80)
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        if (kb >= nkb) break;
+        f32x16 sc[2];
+        scores(kb, sc);
+        read_v(kb, va);
+        softmax(kb, sc, pa);
+        pv(va, pa);
       }
     }
   }
