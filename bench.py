@@ -52,6 +52,10 @@ def parse():
     ap.add_argument("--cpu-configs-budget-s", type=float, default=8.0,
                     help="per-workload time budget of the micro-batch-1 reference timings (0 to skip)")
     ap.add_argument("--sweep-steps", type=int, default=5)
+    ap.add_argument("--serving-s", type=float, default=3.0,
+                    help="seconds of live Poisson arrivals replayed through the micro-batcher (0 to skip)")
+    ap.add_argument("--serving-load", type=float, default=0.7,
+                    help="offered load of the serving runs, as a fraction of the micro-batch-64 capacity")
     ap.add_argument("--cpu-budget-s", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="skip the event-timed roofline pass")
@@ -265,6 +269,96 @@ def cpu_config_timing(preset, wl, budget_s):
     return rec
 
 
+def service_times(rows, pool, bound):
+    """Seconds per micro-batch of b requests, b = 1 .. bound, from the swept
+    pass times (linear between measured sizes)."""
+    bs = [r["micro_batch"] for r in rows]
+    per = [r["ms_per_pass"] * 1e-3 / r["micro_batches_per_pass"] for r in rows]
+    return [0.0] + [float(v) for v in __import__("numpy").interp(range(1, bound + 1), bs, per)]
+
+
+def serving(wl, rows, load, live_s, B=64, p=0.6, max_age=1.0):
+    """The Poisson-gap micro-batcher (Section 3.2) in front of this encoder.
+
+    * replay cost of the library's batcher per arrival (C++);
+    * four dispatch policies on one Poisson trace (the comparison of the
+      paper's Figure 4), and the Poisson-gap rule under Gamma arrivals of CV
+      0.5, 1, 2 (Section 5's sensitivity study), through a single encode
+      server that takes the measured micro-batch times;
+    * a live replay: Poisson arrivals at the same load drive the GPU encoder
+      in real time; latency = batch completion (HIP event) - arrival."""
+    import numpy as np
+    import torch
+    from paper_2609_31551_amd import batcher as L, synth
+    svc = service_times(rows, wl.pool, B)
+    capacity = B / svc[B]
+    lam = load * capacity
+    out = {"batch_bound": B, "fill_prob": p, "max_age_s": max_age, "capacity_items_per_s": capacity,
+           "offered_items_per_s": lam, "gap_s": L.poisson_gap_threshold(B, p, lam)}
+
+    arr = synth.arrival_trace(1000000, lam, 1.0, seed=0)
+    t0 = time.perf_counter()
+    L.batcher_simulate(arr, B, p, lam, max_age, svc)
+    out["replay_ns_per_arrival"] = (time.perf_counter() - t0) / arr.shape[0] * 1e9
+
+    def summarize(arr, r):
+        lat = r["done_t"] - arr
+        span = r["done_t"].max() - arr[0]
+        return {"items_per_s": arr.shape[0] / span, "latency_mean_ms": float(lat.mean() * 1e3),
+                "latency_p99_ms": float(np.percentile(lat, 99) * 1e3),
+                "mean_batch": float(arr.shape[0] / r["n_batches"]), "batches": int(r["n_batches"])}
+
+    arr = synth.arrival_trace(20000, lam, 1.0, seed=1)
+    never = 1.0 - 1e-12       # p -> 1: the idle-gap condition never fires
+    policies = {"fixed_bound_no_timeout": (never, 1e9), "timeout_2ms": (never, 0.002),
+                "timeout_50ms": (never, 0.05), "poisson_gap": (p, max_age)}
+    out["policies_cv1"] = {k: summarize(arr, L.batcher_simulate(arr, B, pp, lam, a, svc))
+                           for k, (pp, a) in policies.items()}
+    out["poisson_gap_vs_cv"] = {}
+    for cv in (0.5, 1.0, 2.0):
+        arr = synth.arrival_trace(20000, lam, cv, seed=2)
+        out["poisson_gap_vs_cv"]["cv%.1f" % cv] = summarize(arr, L.batcher_simulate(arr, B, p, lam, max_age, svc))
+
+    if live_s > 0:
+        arr = synth.arrival_trace(max(1, int(lam * live_s)), lam, 1.0, seed=3)
+        bt = L.Batcher(B, p, lam, max_age)
+        recs = []
+
+        def dispatch():
+            ids, _ = bt.take()
+            items = [wl.items[j % wl.pool] for j in ids]
+            with torch.cuda.stream(wl.stream):
+                packed, cu, grid = wl.enc.pack_microbatch(items, stream=wl.stream)
+                wl.enc.encode_microbatch(packed, cu, None if wl.whisper else grid, wl.wdev,
+                                         out=wl.out[:wl.enc.out_rows(cu)], stream=wl.stream)
+                ev = torch.cuda.Event(enable_timing=True)
+                ev.record(wl.stream)
+            recs.append((ids, ev))
+
+        torch.cuda.synchronize()
+        ev0 = torch.cuda.Event(enable_timing=True)
+        ev0.record(wl.stream)
+        start = time.perf_counter()
+        i, n = 0, arr.shape[0]
+        while i < n or bt.size():
+            now = time.perf_counter() - start
+            while i < n and arr[i] <= now:
+                if bt.size() and bt.deadline() < arr[i]:
+                    dispatch()
+                if bt.arrive(arr[i], i):
+                    dispatch()
+                i += 1
+            if bt.size() and bt.poll(now):
+                dispatch()
+        torch.cuda.synchronize()
+        done = np.empty(n)
+        for ids, ev in recs:
+            done[ids] = ev0.elapsed_time(ev) * 1e-3
+        r = {"done_t": done, "n_batches": len(recs)}
+        out["live_poisson"] = dict(summarize(arr, r), seconds=float(arr[-1]), requests=int(n))
+    return out
+
+
 def parse_workloads(spec):
     out = []
     for part in spec.split(";"):
@@ -327,6 +421,9 @@ def main():
     if sweep:
         workloads[preset["name"]] = {"pool": pool, "sweep": sweep_rows(wl, sweep, args.sweep_steps,
                                                                        not args.no_profile)}
+    if sweep and args.serving_s >= 0 and max(sweep) == pool and len(sweep) > 1:
+        result["serving"] = serving(wl, workloads[preset["name"]]["sweep"], args.serving_load, args.serving_s,
+                                    B=pool)
     cpu_configs = {}
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(preset, wl, args.batch, args.cpu_budget_s)

@@ -162,3 +162,14 @@ def make_items(cfg, n, seed=0, shapes=None):
     if cfg["dtype"] == "bf16":
         items = [round_to_bf16(a) for a in items]
     return items
+
+
+def arrival_trace(n, rate, cv=1.0, seed=0):
+    """n request arrival times (seconds, from 0) with i.i.d. Gamma
+    inter-arrival gaps of mean 1/rate and coefficient of variation cv
+    (cv = 1: Poisson arrivals).  The arrival patterns of the sensitivity
+    study (Section 5) use cv 0.5, 1 and 2."""
+    rng = np.random.Generator(np.random.PCG64(seed + 2))
+    shape = 1.0 / (cv * cv)
+    gaps = rng.gamma(shape, 1.0 / (rate * shape), size=n)
+    return np.cumsum(gaps) - gaps[0]

@@ -28,6 +28,16 @@ def test_every_declared_symbol_is_exported():
     assert sorted(eas.EXPORTS) == names
 
 
+def test_every_batcher_symbol_is_exported():
+    from paper_2609_31551_amd import batcher
+    text = open(os.path.join(ROOT, "include", "eas_batcher.h")).read()
+    names = sorted(set(re.findall(r"^\s*(?:eas_status|void)\s+(eas_\w+)\s*\(", text, re.M)))
+    assert len(names) == 12
+    for n in names:
+        assert hasattr(eas.LIB, n), n
+    assert list(batcher.EXPORTS) == names
+
+
 @pytest.mark.parametrize("preset", list(C.PRESETS.values()), ids=list(C.PRESETS))
 def test_weight_layout_matches_generator_tensor_list(preset):
     cfg = eas.make_config(C.with_layers(preset, 2), max_tokens=1024)
