@@ -421,6 +421,16 @@ def main():
     if sweep:
         workloads[preset["name"]] = {"pool": pool, "sweep": sweep_rows(wl, sweep, args.sweep_steps,
                                                                        not args.no_profile)}
+    if sweep and len(sweep) > 1:
+        from paper_2609_31551_amd import capacity as K
+        rows = {r["micro_batch"]: r["items_per_s"] for r in workloads[preset["name"]]["sweep"]}
+        doubling = [b for b in sorted(rows) if b & (b - 1) == 0]
+        c_e, b_sat, curve = K.saturation_capacity(lambda b: rows[b], max(doubling))
+        lam = args.serving_load * c_e
+        result["capacity"] = {"c_e_items_per_s": c_e, "b_sat": b_sat, "curve": curve,
+                              "rule": "double B until a doubling gains < 5% (Section 3.1)",
+                              "example_load_items_per_s": lam, "rho_e": K.utilization(lam, 1, c_e),
+                              "b_max": K.batch_cap(lam, 1)}
     if sweep and args.serving_s >= 0 and max(sweep) == pool and len(sweep) > 1:
         result["serving"] = serving(wl, workloads[preset["name"]]["sweep"], args.serving_load, args.serving_s,
                                     B=pool)
