@@ -319,6 +319,35 @@ def serving(wl, rows, load, live_s, B=64, p=0.6, max_age=1.0):
         arr = synth.arrival_trace(20000, lam, cv, seed=2)
         out["poisson_gap_vs_cv"]["cv%.1f" % cv] = summarize(arr, L.batcher_simulate(arr, B, p, lam, max_age, svc))
 
+    # deficit-counter router (Section 3.3): cost per decision, and the device
+    # gather of the micro-batch's output into per-destination envelopes
+    from paper_2609_31551_amd import router as R
+    rt = R.Router(0.7)
+    t0 = time.perf_counter()
+    rt.route(1000000)
+    out["router_ns_per_decision"] = (time.perf_counter() - t0) / 1e6 * 1e9
+    n_req = wl.pool
+    rows = np.array([wl.enc.out_rows([0, t]) for t in wl.item_tokens[:n_req]], np.int64)
+    src_rows = np.concatenate([[0], np.cumsum(rows)])
+    dest = rt.route(n_req).astype(np.int32)
+    _, _, req_rows = R.envelope_plan(dest, 2, rows)
+    src = wl.out[:int(src_rows[-1])]
+    dst = torch.empty_like(src)
+    with torch.cuda.stream(wl.stream):
+        for _ in range(3):
+            R.envelope_gather(src, src_rows, req_rows, dst, stream=wl.stream)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(wl.stream)
+        for _ in range(20):
+            R.envelope_gather(src, src_rows, req_rows, dst, stream=wl.stream)
+        e1.record(wl.stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / 20
+    nbytes = 2 * src.numel() * src.element_size()
+    out["envelope_gather"] = {"requests": n_req, "bytes_moved": nbytes, "ms": ms, "gbs": nbytes / (ms * 1e-3) / 1e9,
+                              "roofline_frac": nbytes / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS,
+                              "note": "encoding in the planned order produces the envelopes with no copy"}
+
     if live_s > 0:
         arr = synth.arrival_trace(max(1, int(lam * live_s)), lam, 1.0, seed=3)
         bt = L.Batcher(B, p, lam, max_age)
@@ -421,11 +450,11 @@ def main():
     if sweep:
         workloads[preset["name"]] = {"pool": pool, "sweep": sweep_rows(wl, sweep, args.sweep_steps,
                                                                        not args.no_profile)}
-    if sweep and len(sweep) > 1:
+    doubling = [1 << i for i in range(max(sweep).bit_length())] if sweep else []
+    if len(doubling) > 1 and set(doubling) <= set(sweep):
         from paper_2609_31551_amd import capacity as K
         rows = {r["micro_batch"]: r["items_per_s"] for r in workloads[preset["name"]]["sweep"]}
-        doubling = [b for b in sorted(rows) if b & (b - 1) == 0]
-        c_e, b_sat, curve = K.saturation_capacity(lambda b: rows[b], max(doubling))
+        c_e, b_sat, curve = K.saturation_capacity(lambda b: rows[b], doubling[-1])
         lam = args.serving_load * c_e
         result["capacity"] = {"c_e_items_per_s": c_e, "b_sat": b_sat, "curve": curve,
                               "rule": "double B until a doubling gains < 5% (Section 3.1)",

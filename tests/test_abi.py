@@ -99,3 +99,13 @@ def test_config_errors_are_reported_without_hip():
         eas.weights_layout(eas.make_config(dict(C.QWEN_IMAGE, rope_sections=(0, 20, 19)), max_tokens=10))
     with pytest.raises(eas.EasError):
         eas.microbatch_shape(eas.make_config(C.QWEN_IMAGE, max_tokens=10 ** 6), [[2, 3, 230, 308]])
+
+
+def test_every_router_symbol_is_exported():
+    from paper_2609_31551_amd import router
+    text = open(os.path.join(ROOT, "include", "eas_router.h")).read()
+    names = sorted(set(re.findall(r"^\s*(?:eas_status|void)\s+(eas_\w+)\s*\(", text, re.M)))
+    assert len(names) == 7
+    for n in names:
+        assert hasattr(eas.LIB, n), n
+    assert list(router.EXPORTS) == names
