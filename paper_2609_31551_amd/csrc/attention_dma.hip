@@ -35,6 +35,9 @@ namespace eas {
 namespace {
 
 constexpr int QTILE = 128, KTILE = 64;
+#ifndef ATTN_QB
+#define ATTN_QB 1
+#endif
 
 #pragma clang diagnostic ignored "-Winline-asm"
 __device__ __forceinline__ void dma16(unsigned lds_addr, unsigned voff, const void* gbase) {
@@ -45,16 +48,19 @@ __device__ __forceinline__ void dma16(unsigned lds_addr, unsigned voff, const vo
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
 
-template <int HD>
+template <int HD, int QB_>
 struct AttnCfg {
+  static constexpr int QB = QB_;                   // 32-query blocks per wave
+  static constexpr int NW = QTILE / (32 * QB);     // waves per workgroup
   static constexpr int R = HD / 8;                 // 16-byte chunks per K / V row
   static constexpr int KS = HD / 16;               // 16-wide k-steps of Q K^T
   static constexpr int HB = (HD + 31) / 32;        // 32-row blocks of O^T
   static constexpr int TILE = KTILE * R * 16;      // bytes of one K or V tile
   static constexpr int BUF = 2 * TILE;             // K + V
-  static constexpr int DMA = R / 2;                // DMA instructions per wave per operand per tile
-  // issue both halves' S^T MFMAs ahead of the softmax (needs 2 more score blocks in VGPRs)
-  static constexpr bool OVERLAP = HD <= 64;
+  static constexpr int NDMA = TILE / 1024;         // DMA instructions per operand per tile (= R)
+  static constexpr int DMA = (NDMA + NW - 1) / NW; // per wave (instruction wave + NW*j)
+  // issue both halves' S^T MFMAs ahead of the softmax (needs a second score block per query block)
+  static constexpr bool OVERLAP = QB == 1 || HD <= 64;
   __device__ static int rot(int row) { return R == 8 ? 2 * (row & 3) + ((row >> 2) & 1) : ((row >> 2) & 1); }
   // logical chunk L of row `row` sits at physical chunk phys(row, L)
   __device__ static int phys(int row, int L) { return (L + rot(row)) % R; }
@@ -70,9 +76,9 @@ __device__ __forceinline__ void decode(const AttnWork& w, int tile, int* s0, int
   *q0 = *s0 + (tile - w.tile_start[i]) * QTILE;
 }
 
-template <int HD>
-__global__ __launch_bounds__(128) void attn_bf16_dma_kernel(AttnArgs a, AttnWork w) {
-  using C = AttnCfg<HD>;
+template <int HD, int QB>
+__global__ __launch_bounds__(QTILE / QB * 2) void attn_bf16_dma_kernel(AttnArgs a, AttnWork w) {
+  using C = AttnCfg<HD, QB>;
   extern __shared__ __attribute__((aligned(1024))) char smem[];
   const unsigned lds0 = (unsigned)(size_t)((__attribute__((address_space(3))) char*)smem);
   const int h = blockIdx.x % a.heads;
@@ -84,15 +90,16 @@ __global__ __launch_bounds__(128) void attn_bf16_dma_kernel(AttnArgs a, AttnWork
   const int dq = a.heads * HD;
   const bf16* qkv = static_cast<const bf16*>(a.qkv);
   const float c = a.scale * 1.4426950408889634f;
-  const int qw0 = q0 + wave * 64;            // this wave's first query
+  const int qw0 = q0 + wave * 32 * QB;       // this wave's first query
   const bool active = qw0 < s1;              // uniform per wave
 
-  // ---- DMA of one K + V tile: wave w moves K and V chunks [w*DMA*64, (w+1)*DMA*64) ----
-  // slot s of a tile is 16 bytes at s*16: row s / R, physical chunk s % R.
+  // ---- DMA of one K + V tile: DMA instruction q (1 KB = 64 slots) belongs to
+  // wave q % NW; slot s of a tile is 16 bytes at s*16: row s / R, physical
+  // chunk s % R.
   int drow[C::DMA], dcol[C::DMA];
 #pragma unroll
   for (int j = 0; j < C::DMA; ++j) {
-    const int slot = (wave * C::DMA + j) * 64 + lane;
+    const int slot = min(wave + C::NW * j, C::NDMA - 1) * 64 + lane;
     drow[j] = slot / C::R;
     dcol[j] = h * HD + C::logical(drow[j], slot % C::R) * 8;
   }
@@ -100,16 +107,19 @@ __global__ __launch_bounds__(128) void attn_bf16_dma_kernel(AttnArgs a, AttnWork
     const unsigned base = lds0 + buf * C::BUF;
 #pragma unroll
     for (int j = 0; j < C::DMA; ++j) {
-      const long key = min(k0 + drow[j], s1 - 1);
-      dma16(base + (wave * C::DMA + j) * 1024, (unsigned)((key * a.ldqkv + dq + dcol[j]) * 2), qkv);
-      dma16(base + C::TILE + (wave * C::DMA + j) * 1024, (unsigned)((key * a.ldqkv + 2 * dq + dcol[j]) * 2), qkv);
+      const int q = wave + C::NW * j;
+      if (C::NDMA % C::NW == 0 || q < C::NDMA) {
+        const long key = min(k0 + drow[j], s1 - 1);
+        dma16(base + q * 1024, (unsigned)((key * a.ldqkv + dq + dcol[j]) * 2), qkv);
+        dma16(base + C::TILE + q * 1024, (unsigned)((key * a.ldqkv + 2 * dq + dcol[j]) * 2), qkv);
+      }
     }
   };
 
   // Q fragments: query block qb, k-step ks: lane l holds hd ks*16 + g*8 .. +8 of query l%32
-  bf16x8 qf[2][C::KS];
+  bf16x8 qf[QB][C::KS];
 #pragma unroll
-  for (int qb = 0; qb < 2; ++qb) {
+  for (int qb = 0; qb < QB; ++qb) {
     const int qr = min(qw0 + qb * 32 + l32, s1 - 1);
 #pragma unroll
     for (int ks = 0; ks < C::KS; ++ks)
@@ -118,18 +128,20 @@ __global__ __launch_bounds__(128) void attn_bf16_dma_kernel(AttnArgs a, AttnWork
   // consume the Q loads here, before any DMA is in flight, so the compiler's
   // own wait for them cannot also wait on a prefetch
 #pragma unroll
-  for (int qb = 0; qb < 2; ++qb)
+  for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
     for (int ks = 0; ks < C::KS; ++ks) asm volatile("" :: "v"(qf[qb][ks]));
 
-  f32x16 o[2][C::HB];
+  f32x16 o[QB][C::HB];
 #pragma unroll
-  for (int qb = 0; qb < 2; ++qb)
+  for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
     for (int hb = 0; hb < C::HB; ++hb)
 #pragma unroll
       for (int e = 0; e < 16; ++e) o[qb][hb][e] = 0.0f;
-  float m_run[2] = {-INFINITY, -INFINITY}, l_part[2] = {0.0f, 0.0f};
+  float m_run[QB], l_part[QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) { m_run[qb] = -INFINITY; l_part[qb] = 0.0f; }
 
   // K operand reads: row kb*32 + l32, logical chunk 2ks + g (the rotation only
   // depends on row & 7, i.e. on l32)
@@ -166,14 +178,14 @@ __global__ __launch_bounds__(128) void attn_bf16_dma_kernel(AttnArgs a, AttnWork
     // softmax overlaps the first half's P V MFMAs.
     auto scores = [&](int kb, f32x16* sc) {
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb)
+      for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
         for (int e = 0; e < 16; ++e) sc[qb][e] = 0.0f;
 #pragma unroll
       for (int ks = 0; ks < C::KS; ++ks) {
         const bf16x8 kf = *reinterpret_cast<const bf16x8*>(Kt + kb * 32 * C::R * 16 + kofs[ks]);
 #pragma unroll
-        for (int qb = 0; qb < 2; ++qb)
+        for (int qb = 0; qb < QB; ++qb)
           sc[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[qb][ks], sc[qb], 0, 0, 0);
       }
     };
@@ -202,13 +214,13 @@ __global__ __launch_bounds__(128) void attn_bf16_dma_kernel(AttnArgs a, AttnWork
       const int kh = k0 + kb * 32;
       if (kh + 32 > s1) {
 #pragma unroll
-        for (int qb = 0; qb < 2; ++qb)
+        for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
           for (int e = 0; e < 16; ++e)
             if (kh + (e >> 2) * 8 + g * 4 + (e & 3) >= s1) sc[qb][e] = -INFINITY;
       }
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
+      for (int qb = 0; qb < QB; ++qb) {
         float mx = sc[qb][0];
 #pragma unroll
         for (int e = 1; e < 16; ++e) mx = fmaxf(mx, sc[qb][e]);
@@ -244,13 +256,13 @@ __global__ __launch_bounds__(128) void attn_bf16_dma_kernel(AttnArgs a, AttnWork
 #pragma unroll
         for (int hb = 0; hb < C::HB; ++hb)
 #pragma unroll
-          for (int qb = 0; qb < 2; ++qb)
+          for (int qb = 0; qb < QB; ++qb)
             o[qb][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[ch][hb], pb[qb][ch], o[qb][hb], 0, 0, 0);
     };
 
-    bf16x8 va[2][C::HB], pa[2][2];
+    bf16x8 va[2][C::HB], pa[QB][2];
     if constexpr (C::OVERLAP) {
-      f32x16 sa[2], sb[2];
+      f32x16 sa[QB], sb[QB];
       scores(0, sa);
       if (nkb == 2) scores(1, sb);
       read_v(0, va);
@@ -268,7 +280,7 @@ __global__ __launch_bounds__(128) void attn_bf16_dma_kernel(AttnArgs a, AttnWork
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
         if (kb >= nkb) break;
-        f32x16 sc[2];
+        f32x16 sc[QB];
         scores(kb, sc);
         read_v(kb, va);
         softmax(kb, sc, pa);
@@ -279,7 +291,7 @@ __global__ __launch_bounds__(128) void attn_bf16_dma_kernel(AttnArgs a, AttnWork
 
   if (!active) return;
 #pragma unroll
-  for (int qb = 0; qb < 2; ++qb) {
+  for (int qb = 0; qb < QB; ++qb) {
     const int qi = qw0 + qb * 32 + l32;
     if (qi >= s1) continue;
     const float inv = 1.0f / (l_part[qb] + __shfl_xor(l_part[qb], 32, 64));
@@ -299,10 +311,12 @@ __global__ __launch_bounds__(128) void attn_bf16_dma_kernel(AttnArgs a, AttnWork
   }
 }
 
-template <int HD>
+template <int HD, int QB>
 hipError_t launch_hd(const AttnArgs& a, const AttnWork& w, int total_tiles, hipStream_t s) {
-  constexpr int lds = 2 * AttnCfg<HD>::BUF;
-  hipLaunchKernelGGL((attn_bf16_dma_kernel<HD>), dim3((unsigned)(total_tiles * a.heads)), dim3(128), lds, s, a, w);
+  using C = AttnCfg<HD, QB>;
+  constexpr int lds = 2 * C::BUF;
+  hipLaunchKernelGGL((attn_bf16_dma_kernel<HD, QB>), dim3((unsigned)(total_tiles * a.heads)), dim3(64 * C::NW), lds, s,
+                     a, w);
   return hipGetLastError();
 }
 
@@ -315,8 +329,8 @@ bool attention_dma_supported(const AttnArgs& a, int N) {
 
 hipError_t launch_attention_bf16_dma(const AttnArgs& a, const AttnWork& w, int total_tiles, hipStream_t s,
                                      const char** kname) {
-  if (a.hd == 64) { *kname = "attn_bf16_hd64"; return launch_hd<64>(a, w, total_tiles, s); }
-  if (a.hd == 80) { *kname = "attn_bf16_hd80"; return launch_hd<80>(a, w, total_tiles, s); }
+  if (a.hd == 64) { *kname = "attn_bf16_hd64"; return launch_hd<64, ATTN_QB>(a, w, total_tiles, s); }
+  if (a.hd == 80) { *kname = "attn_bf16_hd80"; return launch_hd<80, ATTN_QB>(a, w, total_tiles, s); }
   return hipErrorInvalidValue;
 }
 
