@@ -75,24 +75,33 @@ def copy_calibration(mib):
     print(json.dumps({"copy_calibration_bytes_read": n * 4, "copy_calibration_bytes_written": n * 4}))
 
 
+# kernel name -> the sources that decide what it reads and writes per launch
+TRAFFIC_SOURCES = {
+    "gemm_bf16_256x256": ("gemm_bf16.hip", "common.h", "eas_api.cpp"),
+    "gemm_bf16_128x128": ("gemm_bf16.hip", "common.h", "eas_api.cpp"),
+    "attn_bf16_hd64": ("attention_dma.hip", "common.h", "eas_api.cpp"),
+    "ln_apply_bf16": ("elementwise.hip", "common.h", "eas_api.cpp"),
+}
+
+
 def traffic_record(kernel):
     """HBM bytes per launch from the committed counter summary, if it was
-    taken on the current kernel source."""
+    taken on the current sources of that kernel."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
-    if not os.path.exists(path):
+    if not os.path.exists(path) or kernel not in TRAFFIC_SOURCES:
         return None
     rec = json.load(open(path)).get(kernel)
     if not rec:
         return None
-    if rec.get("source_sha") != source_sha():
+    if rec.get("source_sha") != source_sha(TRAFFIC_SOURCES[kernel]):
         return None
     return rec.get("bytes_per_launch")
 
 
-def source_sha():
+def source_sha(files):
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2609_31551_amd", "csrc")
-    for f in sorted(os.listdir(csrc)):
+    for f in files:
         h.update(open(os.path.join(csrc, f), "rb").read())
     return h.hexdigest()[:16]
 

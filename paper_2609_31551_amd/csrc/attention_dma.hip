@@ -5,9 +5,9 @@
 //   O = softmax(Q K^T / sqrt(hd)) V, full within the sequence, nothing across.
 //
 // Design (gfx950):
-//  * A workgroup is 2 waves and owns 128 queries of one (sequence, head);
-//    each wave owns 64 queries as two 32-query MFMA column blocks, so every
-//    K / V operand fragment read from LDS feeds two MFMAs.
+//  * A workgroup is 4 waves and owns 128 queries of one (sequence, head);
+//    each wave owns one 32-query MFMA column block (<= 128 VGPRs, so 4 waves
+//    share a SIMD and hide each other's latency).
 //  * K and V tiles of 64 keys arrive by direct DMA (global_load_lds_dwordx4)
 //    into two LDS buffers: tile t+1 streams in while tile t is consumed,
 //    one barrier per tile.  Tiles are anchored at the sequence start; rows
@@ -26,7 +26,7 @@
 //    8-byte row pieces into four columns.
 //  * For head_dim 64, both halves' S^T MFMAs of a 64-key tile are issued
 //    before the first softmax, so the softmax of one half overlaps MFMAs of
-//    the other (head_dim 80 has no registers for the second score block).
+//    the other; head_dim 80 keeps one half's scores live at a time.
 //  * A 32-key half tile that lies wholly past the sequence end is skipped,
 //    and a wave whose queries all lie past the end skips the arithmetic.
 #include "common.h"
@@ -34,10 +34,10 @@
 namespace eas {
 namespace {
 
+// queries per workgroup (4 waves of 32) and keys per K / V tile; larger query
+// tiles share each K / V tile among more queries but measured slower (fewer
+// workgroups per CU)
 constexpr int QTILE = 128, KTILE = 64;
-#ifndef ATTN_QB
-#define ATTN_QB 1
-#endif
 
 #pragma clang diagnostic ignored "-Winline-asm"
 __device__ __forceinline__ void dma16(unsigned lds_addr, unsigned voff, const void* gbase) {
@@ -50,8 +50,9 @@ typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
 
 template <int HD, int QB_>
 struct AttnCfg {
+  static constexpr int QT = QTILE;                 // queries per workgroup
   static constexpr int QB = QB_;                   // 32-query blocks per wave
-  static constexpr int NW = QTILE / (32 * QB);     // waves per workgroup
+  static constexpr int NW = QT / (32 * QB);        // waves per workgroup
   static constexpr int R = HD / 8;                 // 16-byte chunks per K / V row
   static constexpr int KS = HD / 16;               // 16-wide k-steps of Q K^T
   static constexpr int HB = (HD + 31) / 32;        // 32-row blocks of O^T
@@ -59,21 +60,25 @@ struct AttnCfg {
   static constexpr int BUF = 2 * TILE;             // K + V
   static constexpr int NDMA = TILE / 1024;         // DMA instructions per operand per tile (= R)
   static constexpr int DMA = (NDMA + NW - 1) / NW; // per wave (instruction wave + NW*j)
-  // issue both halves' S^T MFMAs ahead of the softmax (needs a second score block per query block)
-  static constexpr bool OVERLAP = QB == 1 || HD <= 64;
+  // Register budget for 4 waves per SIMD (<= 128 VGPRs): head_dim 64 issues both
+  // halves' S^T MFMAs ahead of the softmax (a second score block per query
+  // block); head_dim 80 instead reads each 16-key chunk's V^T fragments right
+  // before its MFMAs.
+  static constexpr bool OVERLAP = HD <= 64;
+  static constexpr bool V_DIRECT = HD > 64;
   __device__ static int rot(int row) { return R == 8 ? 2 * (row & 3) + ((row >> 2) & 1) : ((row >> 2) & 1); }
   // logical chunk L of row `row` sits at physical chunk phys(row, L)
   __device__ static int phys(int row, int L) { return (L + rot(row)) % R; }
   __device__ static int logical(int row, int p) { return (p + R - rot(row)) % R; }
 };
 
-__device__ __forceinline__ void decode(const AttnWork& w, int tile, int* s0, int* s1, int* q0) {
+__device__ __forceinline__ void decode(const AttnWork& w, int tile, int qt, int* s0, int* s1, int* q0) {
   int i = 0;
   while (i + 1 < w.n && w.tile_start[i + 1] <= tile) ++i;
   const int r = w.order[i];
   *s0 = w.cu[r];
   *s1 = w.cu[r + 1];
-  *q0 = *s0 + (tile - w.tile_start[i]) * QTILE;
+  *q0 = *s0 + (tile - w.tile_start[i]) * qt;
 }
 
 template <int HD, int QB>
@@ -83,7 +88,7 @@ __global__ __launch_bounds__(QTILE / QB * 2) void attn_bf16_dma_kernel(AttnArgs 
   const unsigned lds0 = (unsigned)(size_t)((__attribute__((address_space(3))) char*)smem);
   const int h = blockIdx.x % a.heads;
   int s0, s1, q0;
-  decode(w, blockIdx.x / a.heads, &s0, &s1, &q0);
+  decode(w, blockIdx.x / a.heads, C::QT, &s0, &s1, &q0);
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 5, l32 = lane & 31;
@@ -259,6 +264,24 @@ __global__ __launch_bounds__(QTILE / QB * 2) void attn_bf16_dma_kernel(AttnArgs 
           for (int qb = 0; qb < QB; ++qb)
             o[qb][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[ch][hb], pb[qb][ch], o[qb][hb], 0, 0, 0);
     };
+    // the same with each 16-key chunk's V^T fragments read right before its MFMAs
+    auto pv_direct = [&](int kb, bf16x8 (*pb)[2]) {
+#pragma unroll
+      for (int ch = 0; ch < 2; ++ch)
+#pragma unroll
+        for (int hb = 0; hb < C::HB; ++hb) {
+          union { bf16x8 v; v4i16 h[2]; } u;
+#pragma unroll
+          for (int half = 0; half < 2; ++half) {
+            const int rbase = (kb * 32 + 16 * ch + 8 * half) * C::R * 16;
+            u.h[half] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (lds_v4i16*)(lds + buf * C::BUF + C::TILE + rbase + vofs[hb]));
+          }
+#pragma unroll
+          for (int qb = 0; qb < QB; ++qb)
+            o[qb][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(u.v, pb[qb][ch], o[qb][hb], 0, 0, 0);
+        }
+    };
 
     bf16x8 va[2][C::HB], pa[QB][2];
     if constexpr (C::OVERLAP) {
@@ -276,15 +299,20 @@ __global__ __launch_bounds__(QTILE / QB * 2) void attn_bf16_dma_kernel(AttnArgs 
         pv(va, pa);
       }
     } else {
-      // one half's scores live at a time (register budget of head_dim 80)
+      // one half's scores live at a time
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
         if (kb >= nkb) break;
         f32x16 sc[QB];
         scores(kb, sc);
-        read_v(kb, va);
-        softmax(kb, sc, pa);
-        pv(va, pa);
+        if constexpr (C::V_DIRECT) {
+          softmax(kb, sc, pa);
+          pv_direct(kb, pa);
+        } else {
+          read_v(kb, va);
+          softmax(kb, sc, pa);
+          pv(va, pa);
+        }
       }
     }
   }
@@ -322,6 +350,8 @@ hipError_t launch_hd(const AttnArgs& a, const AttnWork& w, int total_tiles, hipS
 
 }  // namespace
 
+int attention_dma_q_tile(int) { return QTILE; }
+
 bool attention_dma_supported(const AttnArgs& a, int N) {
   return (a.hd == 64 || a.hd == 80) && a.ldqkv % 8 == 0 && (uintptr_t)a.qkv % 16 == 0 &&
          (double)N * a.ldqkv * 2 < 4294967296.0;
@@ -329,8 +359,8 @@ bool attention_dma_supported(const AttnArgs& a, int N) {
 
 hipError_t launch_attention_bf16_dma(const AttnArgs& a, const AttnWork& w, int total_tiles, hipStream_t s,
                                      const char** kname) {
-  if (a.hd == 64) { *kname = "attn_bf16_hd64"; return launch_hd<64, ATTN_QB>(a, w, total_tiles, s); }
-  if (a.hd == 80) { *kname = "attn_bf16_hd80"; return launch_hd<80, ATTN_QB>(a, w, total_tiles, s); }
+  if (a.hd == 64) { *kname = "attn_bf16_hd64"; return launch_hd<64, 1>(a, w, total_tiles, s); }
+  if (a.hd == 80) { *kname = "attn_bf16_hd80"; return launch_hd<80, 1>(a, w, total_tiles, s); }
   return hipErrorInvalidValue;
 }
 

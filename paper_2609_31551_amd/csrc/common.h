@@ -94,8 +94,9 @@ struct AttnArgs {
 };
 hipError_t launch_attention_bf16(const AttnArgs& a, const AttnWork& w, int total_tiles, int N, hipStream_t s,
                                  const char** kname);
-// DMA-fed kernel for head_dim 64 / 80 (same 128-query tiles as the staged one)
+// DMA-fed kernel for head_dim 64 / 80, and its queries per work-list tile
 bool attention_dma_supported(const AttnArgs& a, int N);
+int attention_dma_q_tile(int hd);
 hipError_t launch_attention_bf16_dma(const AttnArgs& a, const AttnWork& w, int total_tiles, hipStream_t s,
                                      const char** kname);
 hipError_t launch_attention_f32(const AttnArgs& a, const AttnWork& w, int total_tiles, hipStream_t s,

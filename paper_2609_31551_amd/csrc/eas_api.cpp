@@ -623,7 +623,13 @@ eas_status eas_encode_microbatch(eas_encoder* enc, const void* packed_in, const 
   std::stable_sort(ord.begin(), ord.end(), [&](int a, int b) {
     return cu_seqlens[a + 1] - cu_seqlens[a] > cu_seqlens[b + 1] - cu_seqlens[b];
   });
-  const int qt = attention_q_tile(bf);
+  // queries per work-list tile of the attention kernel that will run
+  AttnArgs probe;
+  std::memset(&probe, 0, sizeof(probe));
+  probe.qkv = enc->qkv;
+  probe.ldqkv = 3 * d;
+  probe.hd = hd;
+  const int qt = bf && attention_dma_supported(probe, N) ? attention_dma_q_tile(hd) : attention_q_tile(bf);
   int tiles = 0;
   double attn_flops = 0.0;
   for (int i = 0; i < n_seqs; ++i) {
