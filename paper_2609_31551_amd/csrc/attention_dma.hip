@@ -66,6 +66,10 @@ struct AttnCfg {
   // before its MFMAs.
   static constexpr bool OVERLAP = HD <= 64;
   static constexpr bool V_DIRECT = HD > 64;
+  // The last O^T block has HB*32 - HD padding rows (16 for head_dim 80): fed
+  // with ones instead of V, they accumulate each query's softmax row sum in
+  // the MFMA (element 8 of every lane lands on row HD or HD + 4).
+  static constexpr bool MFMA_SUM = HB * 32 - HD >= 16;
   __device__ static int rot(int row) { return R == 8 ? 2 * (row & 3) + ((row >> 2) & 1) : ((row >> 2) & 1); }
   // logical chunk L of row `row` sits at physical chunk phys(row, L)
   __device__ static int phys(int row, int L) { return (L + rot(row)) % R; }
@@ -194,6 +198,11 @@ __global__ __launch_bounds__(QTILE / QB * 2) void attn_bf16_dma_kernel(AttnArgs 
           sc[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[qb][ks], sc[qb], 0, 0, 0);
       }
     };
+    // lanes whose V^T fragment rows lie past HD in the last block (MFMA_SUM)
+    const bool pad_lane = C::MFMA_SUM && (lane & 31) >= HD - (C::HB - 1) * 32;
+    bf16x8 ones;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) ones[e] = (bf16)1.0f;
     // V^T operand fragments of half kb: [ch][hb], 16 keys each
     auto read_v = [&](int kb, bf16x8 (*va)[C::HB]) {
 #pragma unroll
@@ -207,7 +216,7 @@ __global__ __launch_bounds__(QTILE / QB * 2) void attn_bf16_dma_kernel(AttnArgs 
             u.h[half] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
                 (lds_v4i16*)(lds + buf * C::BUF + C::TILE + rbase + vofs[hb]));
           }
-          va[ch][hb] = u.v;
+          va[ch][hb] = (hb == C::HB - 1 && pad_lane) ? ones : u.v;
         }
     };
     // Online softmax.  Scores are masked only in a half that reaches past the
@@ -249,10 +258,10 @@ __global__ __launch_bounds__(QTILE / QB * 2) void attn_bf16_dma_kernel(AttnArgs 
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const float p = __builtin_amdgcn_exp2f(fmaf(sc[qb][e], c, nm));
-          psum += p;
+          if constexpr (!C::MFMA_SUM) psum += p;
           pb[qb][e >> 3][e & 7] = (bf16)p;
         }
-        l_part[qb] += psum;
+        if constexpr (!C::MFMA_SUM) l_part[qb] += psum;
       }
     };
     auto pv = [&](bf16x8 (*va)[C::HB], bf16x8 (*pb)[2]) {
@@ -277,9 +286,10 @@ __global__ __launch_bounds__(QTILE / QB * 2) void attn_bf16_dma_kernel(AttnArgs 
             u.h[half] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
                 (lds_v4i16*)(lds + buf * C::BUF + C::TILE + rbase + vofs[hb]));
           }
+          const bf16x8 vv = (hb == C::HB - 1 && pad_lane) ? ones : u.v;
 #pragma unroll
           for (int qb = 0; qb < QB; ++qb)
-            o[qb][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(u.v, pb[qb][ch], o[qb][hb], 0, 0, 0);
+            o[qb][hb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vv, pb[qb][ch], o[qb][hb], 0, 0, 0);
         }
     };
 
@@ -322,7 +332,8 @@ __global__ __launch_bounds__(QTILE / QB * 2) void attn_bf16_dma_kernel(AttnArgs 
   for (int qb = 0; qb < QB; ++qb) {
     const int qi = qw0 + qb * 32 + l32;
     if (qi >= s1) continue;
-    const float inv = 1.0f / (l_part[qb] + __shfl_xor(l_part[qb], 32, 64));
+    const float inv = C::MFMA_SUM ? 1.0f / o[qb][C::HB - 1][8]
+                                  : 1.0f / (l_part[qb] + __shfl_xor(l_part[qb], 32, 64));
     bf16* out = static_cast<bf16*>(a.out) + (long)qi * a.ldo + h * HD;
 #pragma unroll
     for (int hb = 0; hb < C::HB; ++hb)
