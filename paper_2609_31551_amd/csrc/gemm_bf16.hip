@@ -29,8 +29,11 @@
 //    accumulators, then every lane owns 8 consecutive columns of a row and
 //    applies bias, GELU / QuickGELU, a position-table row and the fp32
 //    residual before one 16-byte (bf16) or 2 x 16-byte (fp32) store.
+//  * Bias / activation epilogues with up to 2048-wide k run a persistent
+//    variant (below) whose epilogue stores keep draining while the next
+//    tile's k-loop runs.
 //  * Every output element accumulates k in the same order (16-wide MFMA
-//    slices, ascending) whatever the tile shape or M, so a
+//    slices, ascending) whatever the kernel, tile shape or M, so a
 //    request's result does not depend on what else is in the micro-batch.
 #include "common.h"
 
@@ -38,6 +41,7 @@ namespace eas {
 namespace {
 
 constexpr int BK = 64, ST = 2;
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
 // M0 carries the LDS base of each DMA; nothing else in these kernels uses M0
 // (checked in the generated code), so setting it here cannot disturb the
@@ -303,6 +307,261 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_tile_kernel(GemmArgs
   }
 }
 
+// ---- persistent variant with an asynchronous epilogue (bias and activation only) ----
+//
+// A fixed grid of workgroups walks the tile list (block b takes tiles b, b + grid,
+// ...; the same XCD-aware order as above), so a CU moves to its next tile
+// without a relaunch: that tile's k-tile 0 streams in under the last k-step and
+// its k-tile 1 under the epilogue.  The epilogue issues no load the compiler
+// knows of -- the bias row reaches LDS by DMA with the operands -- and writes
+// through buffer stores whose count per wave is fixed (lanes outside the
+// output get an out-of-range offset and are dropped by the buffer unit), so the
+// next tile's waits can count past them: vector memory operations complete in
+// issue order, and the stores keep draining while the next tile's k-loop runs.
+// The MFMA operands are swapped (C^T blocks: each lane holds 4 consecutive
+// columns of one row), so a 32 x 32 block reaches the per-wave staging slab
+// with 16-byte writes.  The products and their order over k are the same as in
+// the kernel above, so the two kernels give identical bits.
+template <int BM, int BN, int WGM, int WGN>
+struct ACfg : Cfg<BM, BN, WGM, WGN> {
+  static constexpr int SLAB = 32 * 32 * 4;                        // per-wave epilogue slab
+  static constexpr int LDS = 2 * Cfg<BM, BN, WGM, WGN>::STAGE + Cfg<BM, BN, WGM, WGN>::NW * SLAB;
+  static_assert(Cfg<BM, BN, WGM, WGN>::WN <= 512, "bias row fits one DMA");
+};
+
+template <int BM, int BN, int WGM, int WGN, int OUTF32>
+__global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_async_kernel(GemmArgs a, int n_tiles) {
+  using C = ACfg<BM, BN, WGM, WGN>;
+  constexpr int S = C::FM * C::FN * 2 * (OUTF32 ? 2 : 1);   // buffer stores per wave per tile
+  static_assert(C::DPS + S + 1 < 64, "vmcnt range");
+  extern __shared__ __attribute__((aligned(1024))) char smem[];
+  const unsigned lds0 = (unsigned)(size_t)((__attribute__((address_space(3))) char*)smem);
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / WGN, wn = wave % WGN;
+  const int tiles_m = (a.M + BM - 1) / BM, tiles_n = (a.N + BN - 1) / BN;
+  const int KT = a.K / BK;   // >= 2
+  const bf16* A = static_cast<const bf16*>(a.A);
+  const bf16* B = static_cast<const bf16*>(a.B);
+  const bf16* bias = a.bias ? static_cast<const bf16*>(a.bias) : B;
+  const float bias_on = a.bias ? 1.0f : 0.0f;
+  const int rr = lane / C::CPR, pch = lane % C::CPR;
+  unsigned a_off[C::DA], b_off[C::DB];
+  auto set_offsets = [&](int m0, int n0) {
+#pragma unroll
+    for (int j = 0; j < C::DA; ++j) {
+      const int r = (wave * C::DA + j) * C::RPI + rr;
+      a_off[j] = (unsigned)(((long)min(m0 + r, a.M - 1) * a.lda + (pch ^ C::sw(r)) * 8) * 2);
+    }
+#pragma unroll
+    for (int j = 0; j < C::DB; ++j) {
+      const int r = (wave * C::DB + j) * C::RPI + rr;
+      b_off[j] = (unsigned)(((long)min(n0 + r, a.N - 1) * a.ldb + (pch ^ C::sw(r)) * 8) * 2);
+    }
+  };
+  auto issue = [&](int kt, int st) {
+    const unsigned base = lds0 + st * C::STAGE;
+#pragma unroll
+    for (int j = 0; j < C::DA; ++j) dma16(base + (wave * C::DA + j) * 1024, a_off[j], A + kt * BK);
+#pragma unroll
+    for (int j = 0; j < C::DB; ++j) dma16(base + C::TA + (wave * C::DB + j) * 1024, b_off[j], B + kt * BK);
+  };
+  auto tile_of = [&](int t, int& m0, int& n0) {
+    int mi, ni;
+    tile_coords(xcd_tile(t, n_tiles), tiles_m, tiles_n, mi, ni);
+    m0 = mi * BM;
+    n0 = ni * BN;
+  };
+  const unsigned slab_lds = lds0 + 2 * C::STAGE + wave * C::SLAB;
+  char* slab_b = smem + 2 * C::STAGE + wave * C::SLAB;
+  float* slab = reinterpret_cast<float*>(slab_b);
+  // this wave's WN bias values -> slab bytes [0, 2 WN); the other lanes repeat them
+  auto issue_bias = [&](int n0) {
+    const int n = a.bias ? min(n0 + wn * C::WN + (lane % (C::WN / 8)) * 8, a.N - 8) : 0;
+    dma16(slab_lds, (unsigned)(n * 2), bias);
+  };
+
+  const int lrow = lane & 31, g = lane >> 5, swz = C::sw(lrow);
+  const int a_row = (wm * C::WM + lrow) * BK * 2, b_row = (wn * C::WN + lrow) * BK * 2;
+  constexpr int NH = BK / 16;
+  int cofs[NH];
+#pragma unroll
+  for (int h = 0; h < NH; ++h) cofs[h] = ((2 * h + g) ^ swz) << 4;
+  f32x16 acc[C::FM][C::FN];
+  bf16x8 fa[2][C::FM], fb[2][C::FN];
+  auto load_frags = [&](int st, int cofs, bf16x8* fa, bf16x8* fb) {
+    const char* As = smem + st * C::STAGE;
+    const char* Bs = As + C::TA;
+#pragma unroll
+    for (int i = 0; i < C::FM; ++i) fa[i] = *reinterpret_cast<const bf16x8*>(As + a_row + i * 32 * BK * 2 + cofs);
+#pragma unroll
+    for (int j = 0; j < C::FN; ++j) fb[j] = *reinterpret_cast<const bf16x8*>(Bs + b_row + j * 32 * BK * 2 + cofs);
+  };
+  auto mma = [&](const bf16x8* fa, const bf16x8* fb) {
+#pragma unroll
+    for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+      for (int j = 0; j < C::FN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[j], fa[i], acc[i][j], 0, 0, 0);
+  };
+  auto interleave = [&]() {
+    constexpr int NR = C::FM + C::FN, NM = C::FM * C::FN;
+    static_assert(NM >= NR, "more reads than MFMAs per slice");
+#pragma unroll
+    for (int i = 0; i < NR; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, NM - NR, 0);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  const int es = OUTF32 ? 4 : 2;
+  const int act = a.act;
+
+  int t = blockIdx.x, m0, n0;
+  tile_of(t, m0, n0);
+  set_offsets(m0, n0);
+  issue(0, 0);
+  issue(1, 1);
+  int sb = 0;          // stage of this tile's k-tile 0
+  bool first = true;
+  for (;;) {
+    const int tn = t + gridDim.x;
+    const bool has_next = tn < n_tiles;
+    int m0n = 0, n0n = 0;
+    if (has_next) tile_of(tn, m0n, n0n);
+    // k-tile 0: issued ahead of k-tile 1 and of the previous tile's S stores
+    if (first) wait_vm<C::DPS>();
+    else wait_vm<C::DPS + S>();
+    __builtin_amdgcn_s_barrier();
+    issue_bias(n0);
+#pragma unroll
+    for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+      for (int j = 0; j < C::FN; ++j)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+    load_frags(sb, cofs[0], fa[0], fb[0]);
+    for (int kt = 0; kt < KT - 1; ++kt) {
+      const int st = (sb + kt) & 1;
+#pragma unroll
+      for (int h = 0; h < NH - 1; ++h) {
+        load_frags(st, cofs[h + 1], fa[(h + 1) & 1], fb[(h + 1) & 1]);
+        mma(fa[h & 1], fb[h & 1]);
+        interleave();
+      }
+      wait_lds();
+      // k-tile kt+1 has landed; at kt == 0 the previous stores and the bias DMA may follow it
+      if (kt == 0) {
+        if (first) wait_vm<1>();
+        else wait_vm<S + 1>();
+      } else {
+        wait_vm<0>();
+      }
+      __builtin_amdgcn_s_barrier();
+      if (kt + 2 < KT) {
+        issue(kt + 2, st);
+      } else if (has_next) {
+        set_offsets(m0n, n0n);
+        issue(0, st);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      load_frags(st ^ 1, cofs[0], fa[NH & 1], fb[NH & 1]);
+      mma(fa[(NH - 1) & 1], fb[(NH - 1) & 1]);
+      interleave();
+    }
+    {
+      const int st = (sb + KT - 1) & 1;
+#pragma unroll
+      for (int h = 0; h < NH - 1; ++h) {
+        load_frags(st, cofs[h + 1], fa[(h + 1) & 1], fb[(h + 1) & 1]);
+        mma(fa[(h) & 1], fb[(h) & 1]);
+        interleave();
+      }
+      mma(fa[(NH - 1) & 1], fb[(NH - 1) & 1]);
+    }
+    wait_lds();
+    // the bias has landed: with KT > 2 the wait of k-step 1 covered it; with KT == 2
+    // only the next tile's k-tile 0 was issued after it
+    if (KT == 2) {
+      if (has_next) wait_vm<C::DPS>();
+      else wait_vm<0>();
+    }
+    __builtin_amdgcn_s_barrier();   // every wave is past the last stage
+    if (has_next) issue(1, (sb + KT + 1) & 1);
+    __builtin_amdgcn_sched_barrier(0);
+
+    // ---- epilogue: one 32 x 32 block at a time through the wave's slab ----
+    const int rows = min(BM, a.M - m0);
+    const __amdgpu_buffer_rsrc_t out_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+        static_cast<char*>(a.out) + (size_t)m0 * a.ldo * es, 0, rows * a.ldo * es, 0x00020000);
+    const int prow = lane >> 2, pc = (lane & 3) * 8;
+    uint4 bq[C::FN];
+#pragma unroll
+    for (int j = 0; j < C::FN; ++j) bq[j] = *reinterpret_cast<const uint4*>(slab_b + (j * 32 + pc) * 2);
+    wait_lds();
+#pragma unroll
+    for (int i = 0; i < C::FM; ++i) {
+#pragma unroll
+      for (int j = 0; j < C::FN; ++j) {
+        // acc element 4q + e sits at row lrow, column 8q + 4g + e of the block
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          *reinterpret_cast<float4*>(slab + lrow * 32 + (((2 * q + g) ^ swz) << 2)) =
+              make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+        wait_lds();
+        const int n = n0 + wn * C::WN + j * 32 + pc;
+        float bv[8];
+        {
+          union { uint4 u; bf16 h[8]; } bb;
+          bb.u = bq[j];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) bv[e] = (float)bb.h[e] * bias_on;
+        }
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+          const int r = p * 16 + prow, mr = wm * C::WM + i * 32 + r;   // row within the tile
+          const int sw = C::sw(r);
+          const float4 s0 = *reinterpret_cast<const float4*>(slab + r * 32 + (((pc >> 2) ^ sw) << 2));
+          const float4 s1 = *reinterpret_cast<const float4*>(slab + r * 32 + ((((pc >> 2) + 1) ^ sw) << 2));
+          float v[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[e] += bv[e];
+          if (act == ACT_GELU) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) v[e] = gelu_erf(v[e]);
+          } else if (act == ACT_QUICKGELU) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) v[e] = quick_gelu(v[e]);
+          }
+          // rows past M fall outside the buffer's range; columns past N are sent out of range
+          const unsigned off = n < a.N ? (unsigned)((mr * a.ldo + n) * es) : 0x80000000u;
+          if (OUTF32) {
+            __builtin_amdgcn_raw_buffer_store_b128(
+                (u32x4){__float_as_uint(v[0]), __float_as_uint(v[1]), __float_as_uint(v[2]), __float_as_uint(v[3])},
+                out_rsrc, off, 0, 0);
+            __builtin_amdgcn_raw_buffer_store_b128(
+                (u32x4){__float_as_uint(v[4]), __float_as_uint(v[5]), __float_as_uint(v[6]), __float_as_uint(v[7])},
+                out_rsrc, off + 16, 0, 0);
+          } else {
+            union { u32x4 u; bf16 h[8]; } pk;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) pk.h[e] = (bf16)v[e];
+            __builtin_amdgcn_raw_buffer_store_b128(pk.u, out_rsrc, off, 0, 0);
+          }
+        }
+      }
+    }
+    if (!has_next) break;
+    wait_lds();   // the slab reads are done before the next bias DMA rewrites it
+    first = false;
+    sb = (sb + KT) & 1;
+    t = tn;
+    m0 = m0n;
+    n0 = n0n;
+  }
+}
+
 template <int BM, int BN, int WGM, int WGN>
 hipError_t launch_tile(const GemmArgs& a, hipStream_t s) {
   using C = Cfg<BM, BN, WGM, WGN>;
@@ -318,6 +577,34 @@ hipError_t launch_tile(const GemmArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+template <int BM, int BN, int WGM, int WGN, int OUTF32>
+hipError_t launch_async_t(const GemmArgs& a, hipStream_t s) {
+  using C = ACfg<BM, BN, WGM, WGN>;
+  auto kern = gemm_bf16_async_kernel<BM, BN, WGM, WGN, OUTF32>;
+  static int slots = 0;   // co-resident workgroups on this device, found once per instantiation
+  if (!slots) {
+    hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
+    if (e != hipSuccess) return e;
+    int dev = 0, cus = 0, per_cu = 0;
+    if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
+    if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
+    if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, (const void*)kern, C::NT, C::LDS)) != hipSuccess)
+      return e;
+    if (per_cu < 1) return hipErrorInvalidConfiguration;
+    slots = cus * per_cu;
+  }
+  const long tiles = (long)((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
+  if (tiles == 0) return hipSuccess;
+  const int grid = (int)(tiles < slots ? tiles : slots);
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(C::NT), C::LDS, s, a, (int)tiles);
+  return hipGetLastError();
+}
+
+template <int BM, int BN, int WGM, int WGN>
+hipError_t launch_async(const GemmArgs& a, hipStream_t s) {
+  return a.out_f32 ? launch_async_t<BM, BN, WGM, WGN, 1>(a, s) : launch_async_t<BM, BN, WGM, WGN, 0>(a, s);
+}
+
 bool al16(const void* p) { return (uintptr_t)p % 16 == 0; }
 
 // The DMA tile kernel's requirements: 16-byte aligned operand rows, K a
@@ -331,6 +618,11 @@ bool tile_ok(const GemmArgs& a) {
   if (a.pos && (!al16(a.pos) || (a.pos_f32 ? a.ld_pos % 4 : a.ld_pos % 8))) return false;
   return true;
 }
+
+// The persistent asynchronous-epilogue kernel: bias / activation epilogues, two
+// to 32 k-tiles.  Past that the epilogue is a small share of a tile and the
+// per-tile kernel measured slightly faster (both give the same bits).
+bool async_ok(const GemmArgs& a) { return tile_ok(a) && !a.resid && !a.pos && a.K >= 2 * BK && a.K <= 32 * BK; }
 
 }  // namespace
 
@@ -368,6 +660,11 @@ hipError_t launch_gemm_bf16(const GemmArgs& a, hipStream_t s, const char** kname
   if (!tile_ok(a)) return launch_gemm_bf16_staged(a, s, kname);
   // Pick the tile by estimated time.  All tiles sum k in the same order, so
   // the choice never changes a result.
+  if (async_ok(a)) switch (best_tile(a.M, a.N, nullptr)) {
+      case 0: *kname = "gemm_bf16_async_256x256"; return launch_async<256, 256, 4, 2>(a, s);
+      case 1: *kname = "gemm_bf16_async_256x128"; return launch_async<256, 128, 4, 2>(a, s);
+      default: *kname = "gemm_bf16_async_128x128"; return launch_async<128, 128, 2, 2>(a, s);
+    }
   switch (best_tile(a.M, a.N, nullptr)) {
     case 0: *kname = "gemm_bf16_256x256"; return launch_tile<256, 256, 4, 2>(a, s);
     case 1: *kname = "gemm_bf16_256x128"; return launch_tile<256, 128, 4, 2>(a, s);
