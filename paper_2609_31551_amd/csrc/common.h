@@ -111,6 +111,8 @@ hipError_t launch_rope(void* qkv, int ldqkv, int N, int heads, int hd, int is_bf
                        const float* inv_freq, const int* slot_axis, hipStream_t s);
 hipError_t launch_cls(const SeqMeta& m, float* x, int d, const void* cls, const void* pos0, int w_bf16,
                       hipStream_t s);
+// [rows, k] 16-bit rows copied to [rows, kp] (kp % 8 == 0, dst 16-byte aligned), zero-filled past k.
+hipError_t launch_pad_cols16(const void* src, int rows, int k, int kp, void* dst, hipStream_t s);
 hipError_t launch_im2col_k3(const void* src, int frames_in, int C, int n_clips, int stride, int is_bf16,
                             void* dst, hipStream_t s);
 

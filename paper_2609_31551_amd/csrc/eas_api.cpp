@@ -232,6 +232,8 @@ struct eas_encoder {
   float* sinus = nullptr;    // [n_frames/2, d] (WHISPER)
   float* inv_freq = nullptr; // [head_dim/2] (VIT_ROPE)
   int* slot_axis = nullptr;  // [head_dim/2]
+  int kpad = 0;              // bf16 ViT with a patch row of k_patch % 64 != 0: k_patch rounded up to 64
+  void* patch_w = nullptr;   // patch weight [hidden, kpad], zero columns past k_patch (bf16)
   std::string err;
   bool prof = false;
   std::vector<ProfRec> recs;
@@ -440,9 +442,13 @@ eas_status eas_encoder_create(const eas_config* cfg, eas_encoder** out) {
   }
   auto al = [](int64_t b) { return (b + 255) / 256 * 256; };
   const int64_t half = d / c.heads / 2;
-  int64_t sz[10] = {al(N * d * 4), al(N * 8), al(qkv_rows * 3 * d * el), al(ao_rows * d * el), al(N * hw * el),
+  // bf16 ViTs whose patch row is not a whole number of 64-element k-tiles run the
+  // embedding GEMM on zero-padded copies (rows in hbuf, weight in patch_w)
+  const int64_t kp = k_patch(c), kpad = (kp + 63) / 64 * 64;
+  if (c.dtype == EAS_BF16 && c.kind != EAS_KIND_WHISPER && kp % 64 && kpad <= hw) e->kpad = (int)kpad;
+  int64_t sz[11] = {al(N * d * 4), al(N * 8), al(qkv_rows * 3 * d * el), al(ao_rows * d * el), al(N * hw * el),
                     al(N * 16), al(N * 4), al(c.kind == EAS_KIND_WHISPER ? (int64_t)c.n_frames / 2 * d * 4 : 256),
-                    al(half * 8 + 256), al(N * d * el)};
+                    al(half * 8 + 256), al(N * d * el), al(e->kpad ? d * kpad * 2 : 0)};
   int64_t total = 0;
   for (int64_t v : sz) total += v;
   if (hipMalloc(&e->ws, total) != hipSuccess) {
@@ -462,6 +468,8 @@ eas_status eas_encoder_create(const eas_config* cfg, eas_encoder** out) {
   e->slot_axis = (int*)(p + al(half * 4));
   p += sz[8];
   e->xn = p;
+  p += sz[9];
+  if (e->kpad) e->patch_w = p;
   hipError_t herr = hipSuccess;
   if (c.kind == EAS_KIND_WHISPER) {   // Whisper-style sinusoid table, computed in double
     const int64_t F = c.n_frames / 2, hc = d / 2;
@@ -662,6 +670,18 @@ eas_status eas_encode_microbatch(eas_encoder* enc, const void* packed_in, const 
   if (vit) {
     const int K = (int)k_patch(c);
     GemmArgs g = gemm_args(N, d, K, packed_in, K, W("patch.w"), K, enc->x, d, 1);
+    if (enc->kpad) {   // zero-padded copies: the patch GEMM runs whole 64-wide k-tiles
+      const int kp = enc->kpad;
+      EAS_TRY(run(enc, s, 0.0, (double)N * (K + kp) * 2, [&](const char** kn) {
+        *kn = "pad_cols";
+        return launch_pad_cols16(packed_in, N, K, kp, enc->hbuf, s);
+      }));
+      EAS_TRY(run(enc, s, 0.0, (double)d * (K + kp) * 2, [&](const char** kn) {
+        *kn = "pad_cols";
+        return launch_pad_cols16(W("patch.w"), d, K, kp, enc->patch_w, s);
+      }));
+      g = gemm_args(N, d, kp, enc->hbuf, kp, enc->patch_w, kp, enc->x, d, 1);
+    }
     g.bias = W("patch.b");
     if (c.kind != EAS_KIND_VIT_ROPE) {
       g.pos = W("pos");

@@ -263,6 +263,19 @@ __global__ void pack_audio_kernel(PackArgs p, int n_mels, int n_frames, T* out) 
   out[idx] = (T)p.src[clip][(long)mel * n_frames + t];
 }
 
+// [rows, k] 16-bit elements -> [rows, kp] with zero columns k .. kp; a thread
+// writes one 16-byte chunk of the output.
+__global__ void pad_cols16_kernel(const uint16_t* src, int rows, int k, int kp, uint16_t* dst) {
+  const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  const int cpr = kp / 8;
+  if (idx >= (long)rows * cpr) return;
+  const int r = (int)(idx / cpr), c0 = (int)(idx % cpr) * 8;
+  union { uint4 u; uint16_t h[8]; } o;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) o.h[e] = c0 + e < k ? src[(long)r * k + c0 + e] : (uint16_t)0;
+  *reinterpret_cast<uint4*>(dst + (long)r * kp + c0) = o.u;
+}
+
 inline unsigned blocks_for(long n, int bs) { return (unsigned)((n + bs - 1) / bs); }
 
 }  // namespace
@@ -319,6 +332,14 @@ hipError_t launch_rope(void* qkv, int ldqkv, int N, int heads, int hd, int is_bf
   else
     hipLaunchKernelGGL((rope_kernel<float>), dim3(blocks_for(total, 256)), dim3(256), 0, s, (float*)qkv, ldqkv, N,
                        heads, hd, pos3, inv_freq, slot_axis);
+  return hipGetLastError();
+}
+
+hipError_t launch_pad_cols16(const void* src, int rows, int k, int kp, void* dst, hipStream_t s) {
+  if (kp % 8 || kp < k || (uintptr_t)dst % 16) return hipErrorInvalidValue;
+  if (rows == 0) return hipSuccess;
+  hipLaunchKernelGGL(pad_cols16_kernel, dim3(blocks_for((long)rows * (kp / 8), 256)), dim3(256), 0, s,
+                     static_cast<const uint16_t*>(src), rows, k, kp, static_cast<uint16_t*>(dst));
   return hipGetLastError();
 }
 
