@@ -40,7 +40,7 @@
 namespace eas {
 namespace {
 
-constexpr int BK = 64, ST = 2;
+constexpr int BK = 64;
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
 // M0 carries the LDS base of each DMA; nothing else in these kernels uses M0
@@ -57,7 +57,7 @@ template <int N> __device__ __forceinline__ void wait_vm() {
 }
 __device__ __forceinline__ void wait_lds() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
-template <int BM, int BN, int WGM, int WGN>
+template <int BM, int BN, int WGM, int WGN, int ST = 2>
 struct Cfg {
   static constexpr int NW = WGM * WGN, NT = 64 * NW;
   static constexpr int WM = BM / WGM, WN = BN / WGN;
@@ -70,7 +70,7 @@ struct Cfg {
   static constexpr int SLD = WN + 4;                            // epilogue slab row (floats)
   static constexpr int LDS = ST * STAGE > NW * 32 * SLD * 4 ? ST * STAGE : NW * 32 * SLD * 4;
   static_assert(BM % (RPI * NW) == 0 && BN % (RPI * NW) == 0, "DMA split");
-  static_assert(DPS < 64, "vmcnt range");
+  static_assert(DPS * (ST - 1) < 64, "vmcnt range");
   // conflict-free chunk swizzle for 128-byte rows: 16 rows per LDS cycle hit 16 distinct 16-byte slots
   __device__ static int sw(int row) { return (row >> 1) & 7; }
 };
@@ -93,9 +93,20 @@ __device__ __forceinline__ void tile_coords(int t, int mt, int nt, int& mi, int&
   mi = g * GROUP_M + r % rows;
 }
 
-template <int BM, int BN, int WGM, int WGN>
+// Waits until at most n k-tiles' DMA (of DPS instructions each) are in flight, 0 <= n <= N.
+template <int DPS, int N>
+__device__ __forceinline__ void wait_tiles(int n) {
+  if constexpr (N > 0) {
+    if (n >= N) { wait_vm<N * DPS>(); return; }
+    wait_tiles<DPS, N - 1>(n);
+  } else {
+    wait_vm<0>();
+  }
+}
+
+template <int BM, int BN, int WGM, int WGN, int ST>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_tile_kernel(GemmArgs a) {
-  using C = Cfg<BM, BN, WGM, WGN>;
+  using C = Cfg<BM, BN, WGM, WGN, ST>;
   extern __shared__ __attribute__((aligned(1024))) char smem[];
   const unsigned lds0 = (unsigned)(size_t)((__attribute__((address_space(3))) char*)smem);
   const int tid = threadIdx.x, lane = tid & 63;
@@ -173,14 +184,14 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_tile_kernel(GemmArgs
   // pin the issue order of one slice: each fragment read of the next slice
   // goes between two MFMAs of this one, so LDS latency hides under the MFMAs
   auto interleave = [&]() {
-    constexpr int NR = C::FM + C::FN, NM = C::FM * C::FN;
-    static_assert(NM >= NR, "more reads than MFMAs per slice");
+    constexpr int NR = C::FM + C::FN, NM = C::FM * C::FN, NP = NR < NM ? NR : NM;
 #pragma unroll
-    for (int i = 0; i < NR; ++i) {
+    for (int i = 0; i < NP; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one LDS read
     }
-    __builtin_amdgcn_sched_group_barrier(0x008, NM - NR, 0);
+    if constexpr (NM > NP) __builtin_amdgcn_sched_group_barrier(0x008, NM - NP, 0);
+    if constexpr (NR > NP) __builtin_amdgcn_sched_group_barrier(0x100, NR - NP, 0);
     __builtin_amdgcn_sched_barrier(0);
   };
 
@@ -188,8 +199,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_tile_kernel(GemmArgs
 #pragma unroll
   for (int s = 0; s < ST; ++s)
     if (s < KT) issue(s, s);
-  if (KT > 1) wait_vm<C::DPS>();   // ST == 2: tile 1 may still be in flight
-  else wait_vm<0>();
+  wait_tiles<C::DPS, ST - 1>(min(ST, KT) - 1);
   __syncthreads();
   load_frags(0, cofs[0], fa[0], fb[0]);
 
@@ -204,10 +214,10 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_tile_kernel(GemmArgs
       interleave();
     }
     // this wave's reads of stage st are done once lgkmcnt drains; tile kt+1
-    // (the newest DMA) has landed at vmcnt 0; after the barrier every wave
-    // is past stage st, which is refilled with tile kt+ST
+    // has landed once only the tiles after it (up to kt+ST-1) are in flight;
+    // after the barrier every wave is past stage st, refilled with tile kt+ST
     wait_lds();
-    wait_vm<0>();
+    wait_tiles<C::DPS, ST - 2>(min(ST - 2, KT - 2 - kt));
     __builtin_amdgcn_s_barrier();
     if (kt + ST < KT) issue(kt + ST, st);
     __builtin_amdgcn_sched_barrier(0);
@@ -562,18 +572,18 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_async_kernel(GemmArg
   }
 }
 
-template <int BM, int BN, int WGM, int WGN>
+template <int BM, int BN, int WGM, int WGN, int ST = 2>
 hipError_t launch_tile(const GemmArgs& a, hipStream_t s) {
-  using C = Cfg<BM, BN, WGM, WGN>;
+  using C = Cfg<BM, BN, WGM, WGN, ST>;
   static bool attr = false;   // raise the dynamic-LDS limit once per instantiation
   if (!attr) {
-    const hipError_t e = hipFuncSetAttribute((const void*)gemm_bf16_tile_kernel<BM, BN, WGM, WGN>,
+    const hipError_t e = hipFuncSetAttribute((const void*)gemm_bf16_tile_kernel<BM, BN, WGM, WGN, ST>,
                                              hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
     if (e != hipSuccess) return e;
     attr = true;
   }
   const long tiles = (long)((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
-  hipLaunchKernelGGL((gemm_bf16_tile_kernel<BM, BN, WGM, WGN>), dim3((unsigned)tiles), dim3(C::NT), C::LDS, s, a);
+  hipLaunchKernelGGL((gemm_bf16_tile_kernel<BM, BN, WGM, WGN, ST>), dim3((unsigned)tiles), dim3(C::NT), C::LDS, s, a);
   return hipGetLastError();
 }
 
@@ -656,10 +666,29 @@ int best_tile(long M, long N, double* t) {
 
 }  // namespace
 
+// Compute units of the current device (queried once).
+int device_cus() {
+  static int cus = 0;
+  if (!cus) {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) == hipSuccess && hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0)
+      cus = n;
+    else
+      return 256;
+  }
+  return cus;
+}
+
 hipError_t launch_gemm_bf16(const GemmArgs& a, hipStream_t s, const char** kname) {
   if (!tile_ok(a)) return launch_gemm_bf16_staged(a, s, kname);
   // Pick the tile by estimated time.  All tiles sum k in the same order, so
   // the choice never changes a result.
+  // Launches that leave CUs idle even with 128 x 128 tiles are latency-bound:
+  // 64 x 128 tiles double the workgroups and keep two k-tiles in flight.
+  if ((long)((a.M + 127) / 128) * ((a.N + 127) / 128) <= device_cus()) {
+    *kname = "gemm_bf16_64x128";
+    return launch_tile<64, 128, 2, 2, 3>(a, s);
+  }
   if (async_ok(a)) switch (best_tile(a.M, a.N, nullptr)) {
       case 0: *kname = "gemm_bf16_async_256x256"; return launch_async<256, 256, 4, 2>(a, s);
       case 1: *kname = "gemm_bf16_async_256x128"; return launch_async<256, 128, 4, 2>(a, s);
