@@ -11,12 +11,14 @@
 //    chunk) assignment applies an XOR swizzle (chunk ^ ((row >> 1) & 7)) that
 //    spreads the MFMA operand reads -- 32 rows at one k offset, 16 lanes per
 //    LDS cycle over 64 banks -- without conflicts.
-//  * Two LDS stages of 64 k: tile k+1 streams in while tile k is consumed.
-//    The DMA is issued from inline assembly so the compiler does not
-//    serialise it against the LDS reads; completion is tracked with explicit
-//    s_waitcnt vmcnt and one workgroup barrier per k-step.
+//  * ST LDS stages of 64 k (two for full launches, three for the small-tile
+//    path of latency-bound ones): tile k+ST-1 streams in while tile k is
+//    consumed.  The DMA is issued from inline assembly so the compiler does
+//    not serialise it against the LDS reads; completion is tracked with
+//    explicit s_waitcnt vmcnt and one workgroup barrier per k-step.
 //  * v_mfma_f32_32x32x16_bf16, each wave a (BM/WGM) x (BN/WGN) sub-tile of
-//    32 x 32 blocks (8 waves of 64 x 128 for the 256 x 256 tile); operand
+//    32 x 32 blocks (16 waves of 64 x 64 for the 256 x 256 tile: four waves
+//    per SIMD keep more stores in flight in the epilogue); operand
 //    fragments for the next 16-wide k slice are read while the current
 //    slice's MFMAs run (the issue order is pinned: one read between two
 //    MFMAs), and the barrier sits before the last slice so its wait overlaps
@@ -695,7 +697,7 @@ hipError_t launch_gemm_bf16(const GemmArgs& a, hipStream_t s, const char** kname
       default: *kname = "gemm_bf16_async_128x128"; return launch_async<128, 128, 2, 2>(a, s);
     }
   switch (best_tile(a.M, a.N, nullptr)) {
-    case 0: *kname = "gemm_bf16_256x256"; return launch_tile<256, 256, 4, 2>(a, s);
+    case 0: *kname = "gemm_bf16_256x256"; return launch_tile<256, 256, 4, 4>(a, s);
     case 1: *kname = "gemm_bf16_256x128"; return launch_tile<256, 128, 4, 2>(a, s);
     default: *kname = "gemm_bf16_128x128"; return launch_tile<128, 128, 2, 2>(a, s);
   }
