@@ -331,19 +331,25 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_tile_kernel(GemmArgs
 // next tile's waits can count past them: vector memory operations complete in
 // issue order, and the stores keep draining while the next tile's k-loop runs.
 // The MFMA operands are swapped (C^T blocks: each lane holds 4 consecutive
-// columns of one row), so a 32 x 32 block reaches the per-wave staging slab
-// with 16-byte writes.  The products and their order over k are the same as in
-// the kernel above, so the two kernels give identical bits.
-template <int BM, int BN, int WGM, int WGN>
+// columns of one row): with bf16 output the bias and activation are applied in
+// registers and a finished 32 x 32 bf16 block reaches the per-wave staging slab
+// with 8-byte writes (2 KB slabs leave room for 16 waves); fp32 sums go through
+// a 4 KB slab with 16-byte writes.  The products, their order over k and the
+// per-element epilogue arithmetic are the same as in the kernel above, so the
+// two kernels give identical bits.
+template <int BM, int BN, int WGM, int WGN, int OUTF32>
 struct ACfg : Cfg<BM, BN, WGM, WGN> {
-  static constexpr int SLAB = 32 * 32 * 4;                        // per-wave epilogue slab
+  // per-wave epilogue slab: a 32 x 32 block of fp32 sums, or of finished bf16
+  // outputs (bias and activation applied in registers first)
+  static constexpr int SLAB = 32 * 32 * (OUTF32 ? 4 : 2);
   static constexpr int LDS = 2 * Cfg<BM, BN, WGM, WGN>::STAGE + Cfg<BM, BN, WGM, WGN>::NW * SLAB;
-  static_assert(Cfg<BM, BN, WGM, WGN>::WN <= 512, "bias row fits one DMA");
+  static_assert(Cfg<BM, BN, WGM, WGN>::WN <= 512 && 1024 <= SLAB, "bias row fits one DMA and the slab");
+  __device__ static int sw16(int row) { return (row >> 2) & 3; }   // 16-byte chunk swizzle of 64-byte rows
 };
 
 template <int BM, int BN, int WGM, int WGN, int OUTF32>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_async_kernel(GemmArgs a, int n_tiles) {
-  using C = ACfg<BM, BN, WGM, WGN>;
+  using C = ACfg<BM, BN, WGM, WGN, OUTF32>;
   constexpr int S = C::FM * C::FN * 2 * (OUTF32 ? 2 : 1);   // buffer stores per wave per tile
   static_assert(C::DPS + S + 1 < 64, "vmcnt range");
   extern __shared__ __attribute__((aligned(1024))) char smem[];
@@ -508,6 +514,50 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_async_kernel(GemmArg
     const __amdgpu_buffer_rsrc_t out_rsrc = __builtin_amdgcn_make_buffer_rsrc(
         static_cast<char*>(a.out) + (size_t)m0 * a.ldo * es, 0, rows * a.ldo * es, 0x00020000);
     const int prow = lane >> 2, pc = (lane & 3) * 8;
+    if constexpr (!OUTF32) {
+      // bf16 output: bias and activation on the sums in place (columns 8q + 4g + e
+      // of each block), then the finished 32 x 32 bf16 block goes through the slab
+      uint2 bq[C::FN][4];
+#pragma unroll
+      for (int j = 0; j < C::FN; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) bq[j][q] = *reinterpret_cast<const uint2*>(slab_b + (j * 32 + 8 * q + 4 * g) * 2);
+      wait_lds();
+#pragma unroll
+      for (int i = 0; i < C::FM; ++i) {
+#pragma unroll
+        for (int j = 0; j < C::FN; ++j) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            union { uint2 u; bf16 h[4]; } bb, pk;
+            bb.u = bq[j][q];
+            float v[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * q + e] + (float)bb.h[e] * bias_on;
+            if (act == ACT_GELU) {
+#pragma unroll
+              for (int e = 0; e < 4; ++e) v[e] = gelu_erf(v[e]);
+            } else if (act == ACT_QUICKGELU) {
+#pragma unroll
+              for (int e = 0; e < 4; ++e) v[e] = quick_gelu(v[e]);
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e) pk.h[e] = (bf16)v[e];
+            *reinterpret_cast<uint2*>(slab_b + lrow * 64 + ((q ^ C::sw16(lrow)) << 4) + g * 8) = pk.u;
+          }
+          wait_lds();
+          const int n = n0 + wn * C::WN + j * 32 + pc;
+#pragma unroll
+          for (int p = 0; p < 2; ++p) {
+            const int r = p * 16 + prow, mr = wm * C::WM + i * 32 + r;   // row within the tile
+            const u32x4 val = *reinterpret_cast<const u32x4*>(slab_b + r * 64 + (((lane & 3) ^ C::sw16(r)) << 4));
+            // rows past M fall outside the buffer's range; columns past N are sent out of range
+            const unsigned off = n < a.N ? (unsigned)((mr * a.ldo + n) * 2) : 0x80000000u;
+            __builtin_amdgcn_raw_buffer_store_b128(val, out_rsrc, off, 0, 0);
+          }
+        }
+      }
+    } else {
     uint4 bq[C::FN];
 #pragma unroll
     for (int j = 0; j < C::FN; ++j) bq[j] = *reinterpret_cast<const uint4*>(slab_b + (j * 32 + pc) * 2);
@@ -564,6 +614,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_async_kernel(GemmArg
         }
       }
     }
+    }
     if (!has_next) break;
     wait_lds();   // the slab reads are done before the next bias DMA rewrites it
     first = false;
@@ -591,7 +642,7 @@ hipError_t launch_tile(const GemmArgs& a, hipStream_t s) {
 
 template <int BM, int BN, int WGM, int WGN, int OUTF32>
 hipError_t launch_async_t(const GemmArgs& a, hipStream_t s) {
-  using C = ACfg<BM, BN, WGM, WGN>;
+  using C = ACfg<BM, BN, WGM, WGN, OUTF32>;
   auto kern = gemm_bf16_async_kernel<BM, BN, WGM, WGN, OUTF32>;
   static int slots = 0;   // co-resident workgroups on this device, found once per instantiation
   if (!slots) {
@@ -692,7 +743,9 @@ hipError_t launch_gemm_bf16(const GemmArgs& a, hipStream_t s, const char** kname
     return launch_tile<64, 128, 2, 2, 3>(a, s);
   }
   if (async_ok(a)) switch (best_tile(a.M, a.N, nullptr)) {
-      case 0: *kname = "gemm_bf16_async_256x256"; return launch_async<256, 256, 4, 2>(a, s);
+      case 0:   // 16 waves of 64 x 64 with bf16 output (2 KB slabs); the fp32 slabs need 8 waves
+        *kname = "gemm_bf16_async_256x256";
+        return a.out_f32 ? launch_async_t<256, 256, 4, 2, 1>(a, s) : launch_async_t<256, 256, 4, 4, 0>(a, s);
       case 1: *kname = "gemm_bf16_async_256x128"; return launch_async<256, 128, 4, 2>(a, s);
       default: *kname = "gemm_bf16_async_128x128"; return launch_async<128, 128, 2, 2>(a, s);
     }
