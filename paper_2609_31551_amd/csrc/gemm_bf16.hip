@@ -737,8 +737,15 @@ hipError_t launch_gemm_bf16(const GemmArgs& a, hipStream_t s, const char** kname
   // Pick the tile by estimated time.  All tiles sum k in the same order, so
   // the choice never changes a result.
   // Launches that leave CUs idle even with 128 x 128 tiles are latency-bound:
-  // 64 x 128 tiles double the workgroups and keep two k-tiles in flight.
-  if ((long)((a.M + 127) / 128) * ((a.N + 127) / 128) <= device_cus()) {
+  // smaller tiles multiply the workgroups and three stages keep two k-tiles in
+  // flight -- 64 x 128 (4 waves of 32 x 64), or 64 x 64 (4 waves of 32 x 32)
+  // while 64 x 128 tiles would leave a quarter of the CUs idle.
+  const int cus = device_cus();
+  if ((long)((a.M + 127) / 128) * ((a.N + 127) / 128) <= cus) {
+    if ((long)((a.M + 63) / 64) * ((a.N + 127) / 128) * 4 <= 3L * cus) {
+      *kname = "gemm_bf16_64x64";
+      return launch_tile<64, 64, 2, 2, 3>(a, s);
+    }
     *kname = "gemm_bf16_64x128";
     return launch_tile<64, 128, 2, 2, 3>(a, s);
   }
