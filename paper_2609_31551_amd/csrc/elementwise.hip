@@ -186,22 +186,35 @@ __global__ void rope_vec_kernel(bf16* qkv, int ldqkv, int N, int heads, int hd, 
     const float pos = (float)(ax == 0 ? p.x : (ax == 1 ? p.y : p.z));
     sincosf(pos * inv_freq[k0 + j], &sn[j], &cs[j]);
   }
-  const int dq = heads * hd;
-  for (int part = 0; part < 2; ++part) {   // q block, then k block
-    for (int h = 0; h < heads; ++h) {
-      bf16* base = qkv + (long)i * ldqkv + part * dq + h * hd + k0;
-      union { uint4 u; bf16 e[8]; } a, c;
-      a.u = *reinterpret_cast<const uint4*>(base);
-      c.u = *reinterpret_cast<const uint4*>(base + half);
-      union { uint4 u; bf16 e[8]; } oa, oc;
+  // head-parts of q (0 .. heads-1) then k (heads .. 2 heads-1), four at a time:
+  // all loads of a group are issued before its stores, so a thread keeps eight
+  // 16-byte loads in flight instead of waiting out one round trip per head
+  constexpr int G = 4;
+  bf16* row = qkv + (long)i * ldqkv + k0;
+  for (int h0 = 0; h0 < 2 * heads; h0 += G) {
+    union { uint4 u; bf16 e[8]; } a[G], c[G];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const float x1 = (float)a.e[j], x2 = (float)c.e[j];
-        oa.e[j] = (bf16)(x1 * cs[j] - x2 * sn[j]);
-        oc.e[j] = (bf16)(x2 * cs[j] + x1 * sn[j]);
+    for (int u = 0; u < G; ++u) {
+      if (h0 + u < 2 * heads) {
+        const bf16* base = row + (h0 + u >= heads ? heads * hd : 0) + ((h0 + u) % heads) * hd;
+        a[u].u = *reinterpret_cast<const uint4*>(base);
+        c[u].u = *reinterpret_cast<const uint4*>(base + half);
       }
-      *reinterpret_cast<uint4*>(base) = oa.u;
-      *reinterpret_cast<uint4*>(base + half) = oc.u;
+    }
+#pragma unroll
+    for (int u = 0; u < G; ++u) {
+      if (h0 + u < 2 * heads) {
+        bf16* base = row + (h0 + u >= heads ? heads * hd : 0) + ((h0 + u) % heads) * hd;
+        union { uint4 u; bf16 e[8]; } oa, oc;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const float x1 = (float)a[u].e[j], x2 = (float)c[u].e[j];
+          oa.e[j] = (bf16)(x1 * cs[j] - x2 * sn[j]);
+          oc.e[j] = (bf16)(x2 * cs[j] + x1 * sn[j]);
+        }
+        *reinterpret_cast<uint4*>(base) = oa.u;
+        *reinterpret_cast<uint4*>(base + half) = oc.u;
+      }
     }
   }
 }
