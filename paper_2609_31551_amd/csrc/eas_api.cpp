@@ -216,6 +216,21 @@ struct ProfRec {
 
 }  // namespace
 
+// Per-token activation buffers of one encode pass: the encoder's workspace, or
+// a row range of it (row r0 onward), so that two halves of a micro-batch can run
+// side by side.  Each buffer holds a fixed number of elements per token, which
+// bounds every use of it (the Whisper front end included).
+struct Workspace {
+  float* x;          // residual stream [tokens, d] fp32
+  float2* stats;     // (mean, rstd) per token
+  void* qkv;         // [tokens, 3d]
+  void* ao;          // [tokens, ao_w]: attention output, Whisper im2col of the mel frames
+  void* hbuf;        // [tokens, hw]: MLP hidden, merger input, padded patch rows, conv2 im2col
+  void* xn;          // LayerNorm output [tokens, d]
+  int4* pos3;        // (t, h, w) per token
+  int* tab_idx;      // learned-position row per token
+};
+
 struct eas_encoder {
   eas_config cfg;
   Layout layout;
@@ -234,6 +249,15 @@ struct eas_encoder {
   int* slot_axis = nullptr;  // [head_dim/2]
   int kpad = 0;              // bf16 ViT with a patch row of k_patch % 64 != 0: k_patch rounded up to 64
   void* patch_w = nullptr;   // patch weight [hidden, kpad], zero columns past k_patch (bf16)
+  int64_t ao_w = 0, hw = 0;  // elements per token of ao and hbuf
+  hipStream_t side = nullptr;                          // second half of a split micro-batch
+  hipEvent_t ev_fork = nullptr, ev_join = nullptr;
+
+  Workspace rows_from(int64_t r0) const {
+    const int64_t d = cfg.hidden, el = cfg.dtype == EAS_BF16 ? 2 : 4;
+    return {x + r0 * d, stats + r0, static_cast<char*>(qkv) + r0 * 3 * d * el, static_cast<char*>(ao) + r0 * ao_w * el,
+            static_cast<char*>(hbuf) + r0 * hw * el, static_cast<char*>(xn) + r0 * d * el, pos3 + r0, tab_idx + r0};
+  }
   std::string err;
   bool prof = false;
   std::vector<ProfRec> recs;
@@ -317,25 +341,25 @@ eas_status gemm_launch(eas_encoder* e, const GemmArgs& g, hipStream_t s) {
 // LN(x) * W^T: fp32 models fuse the LayerNorm into the GEMM's A loader; bf16
 // models write the normalised rows once as bf16 and run the plain GEMM.
 // x is [M * group, dim] fp32 viewed as M rows of group * dim.
-eas_status ln_gemm(eas_encoder* e, GemmArgs g, float eps, int group, hipStream_t s) {
+eas_status ln_gemm(eas_encoder* e, const Workspace& w, GemmArgs g, float eps, int group, hipStream_t s) {
   const int dim = g.ln_dim, rows = g.M * group;
   const float* x = static_cast<const float*>(g.A);
   if (e->cfg.dtype != EAS_BF16) {
     eas_status rc = run(e, s, 0.0, (double)rows * (dim * 4 + 8), [&](const char** kn) {
       *kn = "ln_stats";
-      return launch_ln_stats(x, rows, dim, eps, e->stats, s);
+      return launch_ln_stats(x, rows, dim, eps, w.stats, s);
     });
     if (rc != EAS_OK) return rc;
-    g.stats = e->stats;
+    g.stats = w.stats;
     g.ln_group = group;
     return gemm(e, g, s);
   }
   eas_status rc = run(e, s, 0.0, (double)rows * dim * 6, [&](const char** kn) {
     *kn = "ln_apply_bf16";
-    return launch_ln_apply(x, rows, dim, eps, g.ln_g, g.ln_b, 1, e->xn, 0, s);
+    return launch_ln_apply(x, rows, dim, eps, g.ln_g, g.ln_b, 1, w.xn, 0, s);
   });
   if (rc != EAS_OK) return rc;
-  g.A = e->xn;   // same [M, group * dim] view, now bf16
+  g.A = w.xn;   // same [M, group * dim] view, now bf16
   g.ln_g = g.ln_b = nullptr;
   return gemm(e, g, s);
 }
@@ -343,6 +367,233 @@ eas_status ln_gemm(eas_encoder* e, GemmArgs g, float eps, int group, hipStream_t
 const char* wptr(const void* weights, const eas_encoder* e, const std::string& name) {
   const int64_t off = e->layout.off(name);
   return off < 0 ? nullptr : static_cast<const char*>(weights) + off;
+}
+
+}  // namespace
+
+namespace {
+
+// One encode pass over requests cu_seqlens[0 .. n_seqs] (offsets from this
+// part's first token) on workspace ws, writing out_embeddings from this part's
+// first output row, on stream s.  The caller has checked the batch and prepared
+// the padded patch weight.
+eas_status encode_part(eas_encoder* enc, const Workspace& ws, const void* packed_in, const int32_t* cu_seqlens,
+                       const int32_t* grid_thw, int32_t n_seqs, const void* weights, void* out_embeddings,
+                       hipStream_t s) {
+  const eas_config& c = enc->cfg;
+  const bool bf = c.dtype == EAS_BF16;
+  const int out_f32 = c.out_dtype == EAS_FP32;
+  const int N = cu_seqlens[n_seqs], d = c.hidden, f = c.mlp, H = c.heads, hd = c.head_dim;
+  const int d3 = 3 * d;
+  const int64_t el = bf ? 2 : 4;
+
+  SeqMeta meta;
+  std::memset(&meta, 0, sizeof(meta));
+  meta.n = n_seqs;
+  meta.cls = c.kind == EAS_KIND_VIT_CLS_ABS;
+  meta.merge = c.merge;
+  for (int r = 0; r <= n_seqs; ++r) meta.cu[r] = cu_seqlens[r];
+  if (grid_thw)
+    for (int r = 0; r < n_seqs; ++r)
+      for (int k = 0; k < 3; ++k) meta.thw[r][k] = grid_thw[3 * r + k];
+
+  // attention work list: longest sequences first
+  AttnWork work;
+  std::memset(&work, 0, sizeof(work));
+  work.n = n_seqs;
+  for (int r = 0; r <= n_seqs; ++r) work.cu[r] = cu_seqlens[r];
+  std::vector<int> ord(n_seqs);
+  for (int r = 0; r < n_seqs; ++r) ord[r] = r;
+  std::stable_sort(ord.begin(), ord.end(), [&](int a, int b) {
+    return cu_seqlens[a + 1] - cu_seqlens[a] > cu_seqlens[b + 1] - cu_seqlens[b];
+  });
+  // queries per work-list tile of the attention kernel that will run
+  AttnArgs probe;
+  std::memset(&probe, 0, sizeof(probe));
+  probe.qkv = ws.qkv;
+  probe.ldqkv = 3 * d;
+  probe.hd = hd;
+  const int qt = bf && attention_dma_supported(probe, N) ? attention_dma_q_tile(hd) : attention_q_tile(bf);
+  int tiles = 0;
+  double attn_flops = 0.0;
+  for (int i = 0; i < n_seqs; ++i) {
+    const int r = ord[i];
+    const int L = cu_seqlens[r + 1] - cu_seqlens[r];
+    work.order[i] = r;
+    work.tile_start[i] = tiles;
+    tiles += (L + qt - 1) / qt;
+    attn_flops += 4.0 * (double)L * L * hd * H;
+  }
+  work.tile_start[n_seqs] = tiles;
+
+  auto W = [&](const std::string& n) { return wptr(weights, enc, n); };
+  eas_status rc = EAS_OK;
+#define EAS_TRY(expr)          \
+  do {                         \
+    rc = (expr);               \
+    if (rc != EAS_OK) return rc; \
+  } while (0)
+
+  const bool vit = c.kind != EAS_KIND_WHISPER;
+  const bool need_pos = vit;
+  if (need_pos)
+    EAS_TRY(run(enc, s, 0.0, (double)N * 20, [&](const char** kn) {
+      *kn = "positions";
+      return launch_positions(meta, N, ws.pos3, ws.tab_idx, c.pos_grid[1], s);
+    }));
+
+  // ---- embedding ----
+  if (vit) {
+    const int K = (int)k_patch(c);
+    GemmArgs g = gemm_args(N, d, K, packed_in, K, W("patch.w"), K, ws.x, d, 1);
+    if (enc->kpad) {   // zero-padded copies: the patch GEMM runs whole 64-wide k-tiles
+      const int kp = enc->kpad;
+      EAS_TRY(run(enc, s, 0.0, (double)N * (K + kp) * 2, [&](const char** kn) {
+        *kn = "pad_cols";
+        return launch_pad_cols16(packed_in, N, K, kp, ws.hbuf, s);
+      }));
+      g = gemm_args(N, d, kp, ws.hbuf, kp, enc->patch_w, kp, ws.x, d, 1);
+    }
+    g.bias = W("patch.b");
+    if (c.kind != EAS_KIND_VIT_ROPE) {
+      g.pos = W("pos");
+      g.pos_f32 = !bf;
+      g.ld_pos = d;
+      g.pos_idx = ws.tab_idx;
+    }
+    EAS_TRY(gemm(enc, g, s));
+    if (c.kind == EAS_KIND_VIT_CLS_ABS) {
+      EAS_TRY(run(enc, s, 0.0, (double)n_seqs * d * 4, [&](const char** kn) {
+        *kn = "cls_insert";
+        return launch_cls(meta, ws.x, d, W("cls"), W("pos"), bf, s);
+      }));
+      EAS_TRY(run(enc, s, 0.0, (double)N * d * 8, [&](const char** kn) {
+        *kn = "ln_apply";
+        return launch_ln_apply(ws.x, N, d, c.ln_eps, W("ln_pre.g"), W("ln_pre.b"), bf, ws.x, 1, s);
+      }));
+    }
+  } else {
+    const int nc = n_seqs, F = c.n_frames, C = c.n_mels;
+    // conv1: im2col [nc*F, 3C] (in ao) -> GEMM + GELU -> [nc*F, d] (in qkv)
+    EAS_TRY(run(enc, s, 0.0, (double)nc * F * C * 3 * el * 2, [&](const char** kn) {
+      *kn = "im2col_k3";
+      return launch_im2col_k3(packed_in, F, C, nc, 1, bf, ws.ao, s);
+    }));
+    GemmArgs g1 = gemm_args(nc * F, d, 3 * C, ws.ao, 3 * C, W("conv1.w"), 3 * C, ws.qkv, d, 0);
+    if (!bf) g1.out_f32 = 1;
+    g1.bias = W("conv1.b");
+    g1.act = ACT_GELU;
+    EAS_TRY(gemm(enc, g1, s));
+    // conv2 (stride 2): im2col [nc*F/2, 3d] (in hbuf) -> GEMM + GELU + sinusoid -> x
+    EAS_TRY(run(enc, s, 0.0, (double)nc * (F / 2) * d * 3 * el * 2, [&](const char** kn) {
+      *kn = "im2col_k3";
+      return launch_im2col_k3(ws.qkv, F, d, nc, 2, bf, ws.hbuf, s);
+    }));
+    GemmArgs g2 = gemm_args(N, d, 3 * d, ws.hbuf, 3 * d, W("conv2.w"), 3 * d, ws.x, d, 1);
+    g2.bias = W("conv2.b");
+    g2.act = ACT_GELU;
+    g2.pos = enc->sinus;
+    g2.pos_f32 = 1;
+    g2.ld_pos = d;
+    g2.pos_period = F / 2;
+    EAS_TRY(gemm(enc, g2, s));
+  }
+
+  // ---- layers ----
+  const int act = c.act == EAS_ACT_GELU ? ACT_GELU : ACT_QUICKGELU;
+  const int mid_f32 = bf ? 0 : 1;   // qkv / attention / MLP activations: model dtype
+  for (int l = 0; l < c.layers; ++l) {
+    const std::string p = "layers." + std::to_string(l) + ".";
+    GemmArgs gq = gemm_args(N, d3, d, ws.x, d, W(p + "qkv.w"), d, ws.qkv, d3, mid_f32);
+    gq.ln_g = W(p + "ln1.g");
+    gq.ln_b = W(p + "ln1.b");
+    gq.ln_dim = d;
+    gq.bias = W(p + "qkv.b");
+    EAS_TRY(ln_gemm(enc, ws, gq, c.ln_eps, 1, s));
+    if (c.kind == EAS_KIND_VIT_ROPE)
+      EAS_TRY(run(enc, s, 0.0, (double)N * 2 * d * el * 2 + (double)N * 16, [&](const char** kn) {
+        *kn = "rope";
+        return launch_rope(ws.qkv, d3, N, H, hd, bf, ws.pos3, enc->inv_freq, enc->slot_axis, s);
+      }));
+    AttnArgs aa;
+    aa.qkv = ws.qkv;
+    aa.ldqkv = d3;
+    aa.out = ws.ao;
+    aa.ldo = d;
+    aa.heads = H;
+    aa.hd = hd;
+    aa.scale = (float)(1.0 / std::sqrt((double)hd));
+    EAS_TRY(run(enc, s, attn_flops, (double)N * 4 * d * el, [&](const char** kn) {
+      return bf ? launch_attention_bf16(aa, work, tiles, N, s, kn) : launch_attention_f32(aa, work, tiles, s, kn);
+    }));
+    GemmArgs go = gemm_args(N, d, d, ws.ao, d, W(p + "o.w"), d, ws.x, d, 1);
+    go.bias = W(p + "o.b");
+    go.resid = ws.x;
+    go.ldr = d;
+    EAS_TRY(gemm(enc, go, s));
+    GemmArgs g1 = gemm_args(N, f, d, ws.x, d, W(p + "fc1.w"), d, ws.hbuf, f, mid_f32);
+    g1.ln_g = W(p + "ln2.g");
+    g1.ln_b = W(p + "ln2.b");
+    g1.ln_dim = d;
+    g1.bias = W(p + "fc1.b");
+    g1.act = act;
+    EAS_TRY(ln_gemm(enc, ws, g1, c.ln_eps, 1, s));
+    // the CLS model's output is the final residual stream: the last FC2 writes it directly
+    const bool direct = c.kind == EAS_KIND_VIT_CLS_ABS && l == c.layers - 1;
+    GemmArgs g2 = gemm_args(N, d, f, ws.hbuf, f, W(p + "fc2.w"), f, direct ? out_embeddings : (void*)ws.x, d,
+                            direct ? out_f32 : 1);
+    g2.bias = W(p + "fc2.b");
+    g2.resid = ws.x;
+    g2.ldr = d;
+    EAS_TRY(gemm(enc, g2, s));
+  }
+
+  // ---- connector ----
+  if (c.merge == 2) {
+    const int G = N / 4, d4 = 4 * d;
+    GemmArgs m1 = gemm_args(G, d4, d4, ws.x, d4, W("m1.w"), d4, ws.hbuf, d4, mid_f32);
+    m1.ln_g = W("ln_q.g");
+    m1.ln_b = W("ln_q.b");
+    m1.ln_dim = d;
+    m1.bias = W("m1.b");
+    m1.act = ACT_GELU;
+    EAS_TRY(ln_gemm(enc, ws, m1, c.merger_ln_eps, 4, s));
+    GemmArgs m2 = gemm_args(G, c.out_dim, d4, ws.hbuf, d4, W("m2.w"), d4, out_embeddings, c.out_dim, out_f32);
+    m2.bias = W("m2.b");
+    EAS_TRY(gemm(enc, m2, s));
+  } else if (c.kind == EAS_KIND_WHISPER) {
+    EAS_TRY(run(enc, s, 0.0, (double)N * d * (4 + (out_f32 ? 4 : 2)), [&](const char** kn) {
+      *kn = "ln_apply";
+      return launch_ln_apply(ws.x, N, d, c.ln_eps, W("ln_post.g"), W("ln_post.b"), bf, out_embeddings, out_f32, s);
+    }));
+  } else if (c.layers == 0) {   // CLS model without layers: the embedding is the output
+    if (hipMemcpyAsync(out_embeddings, ws.x, (size_t)N * d * 4, hipMemcpyDeviceToDevice, s) != hipSuccess)
+      return fail(enc, EAS_ERR_HIP, "hipMemcpyAsync failed");
+  }
+#undef EAS_TRY
+  return EAS_OK;
+}
+
+// Large micro-batches are encoded as two halves side by side, requests [0, k)
+// and [k, n) split about evenly by tokens: each half's kernels fill the other's
+// partial GEMM rounds and overlap its memory-bound steps.  A request's result
+// does not depend on the split (every kernel choice gives the same bits).
+// Returns k, or 0 for one pass: per-kernel profiling (one stream of events),
+// small batches, and halves whose buffers would lose 16-byte alignment.
+constexpr int kSplitTokens = 16384;
+int split_point(const eas_encoder* e, const int32_t* cu, int n, int64_t* in_off, int64_t* out_off) {
+  const eas_config& c = e->cfg;
+  if (e->prof || !e->side || n < 2 || cu[n] < kSplitTokens) return 0;
+  int k = 1;
+  while (k < n - 1 && 2 * (int64_t)cu[k] < cu[n]) ++k;
+  const int64_t el = c.dtype == EAS_BF16 ? 2 : 4, oel = c.out_dtype == EAS_FP32 ? 4 : 2, r0 = cu[k];
+  *in_off = c.kind == EAS_KIND_WHISPER ? (int64_t)k * c.n_mels * c.n_frames * el : r0 * k_patch(c) * el;
+  *out_off = (c.merge == 2 ? r0 / 4 : r0) * c.out_dim * oel;
+  const int64_t offs[] = {*in_off, *out_off, r0 * c.hidden * 4, r0 * 3 * c.hidden * el, r0 * e->ao_w * el,
+                          r0 * e->hw * el, r0 * c.hidden * el};
+  for (int64_t o : offs)
+    if (o % 16) return 0;
+  return k;
 }
 
 }  // namespace
@@ -470,6 +721,8 @@ eas_status eas_encoder_create(const eas_config* cfg, eas_encoder** out) {
   e->xn = p;
   p += sz[9];
   if (e->kpad) e->patch_w = p;
+  e->ao_w = ao_rows * d / N;   // >= d, and >= 6 n_mels for Whisper (two im2col frames per token)
+  e->hw = hw;
   hipError_t herr = hipSuccess;
   if (c.kind == EAS_KIND_WHISPER) {   // Whisper-style sinusoid table, computed in double
     const int64_t F = c.n_frames / 2, hc = d / 2;
@@ -494,6 +747,18 @@ eas_status eas_encoder_create(const eas_config* cfg, eas_encoder** out) {
     herr = hipMemcpy(e->inv_freq, inv.data(), inv.size() * 4, hipMemcpyHostToDevice);
     if (herr == hipSuccess) herr = hipMemcpy(e->slot_axis, ax.data(), ax.size() * 4, hipMemcpyHostToDevice);
   }
+  // second stream and fork / join events for split micro-batches (default
+  // priority); without them every call runs as one pass
+  if (herr == hipSuccess && c.max_seqs >= 2) {
+    if (hipStreamCreateWithFlags(&e->side, hipStreamNonBlocking) != hipSuccess) e->side = nullptr;
+    if (e->side && (hipEventCreateWithFlags(&e->ev_fork, hipEventDisableTiming) != hipSuccess ||
+                    hipEventCreateWithFlags(&e->ev_join, hipEventDisableTiming) != hipSuccess)) {
+      if (e->ev_fork) (void)hipEventDestroy(e->ev_fork);
+      (void)hipStreamDestroy(e->side);
+      e->side = nullptr;
+      e->ev_fork = nullptr;
+    }
+  }
   if (herr != hipSuccess) {
     (void)hipFree(e->ws);
     delete e;
@@ -511,6 +776,11 @@ void eas_encoder_destroy(eas_encoder* enc) {
     (void)hipEventDestroy(r.e1);
   }
   for (auto ev : enc->pool) (void)hipEventDestroy(ev);
+  if (enc->side) {
+    (void)hipEventDestroy(enc->ev_fork);
+    (void)hipEventDestroy(enc->ev_join);
+    (void)hipStreamDestroy(enc->side);
+  }
   (void)hipFree(enc->ws);
   delete enc;
 }
@@ -605,200 +875,37 @@ eas_status eas_encode_microbatch(eas_encoder* enc, const void* packed_in, const 
     return fail(enc, EAS_ERR_INVALID_ARG, "current device differs from the handle's device");
 
   hipStream_t s = static_cast<hipStream_t>(stream);
-  const bool bf = c.dtype == EAS_BF16;
-  const int out_f32 = c.out_dtype == EAS_FP32;
-  const int N = cu_seqlens[n_seqs], d = c.hidden, f = c.mlp, H = c.heads, hd = c.head_dim;
-  const int d3 = 3 * d;
-  const int64_t el = bf ? 2 : 4;
-
-  SeqMeta meta;
-  std::memset(&meta, 0, sizeof(meta));
-  meta.n = n_seqs;
-  meta.cls = c.kind == EAS_KIND_VIT_CLS_ABS;
-  meta.merge = c.merge;
-  for (int r = 0; r <= n_seqs; ++r) meta.cu[r] = cu_seqlens[r];
-  if (grid_thw)
-    for (int r = 0; r < n_seqs; ++r)
-      for (int k = 0; k < 3; ++k) meta.thw[r][k] = grid_thw[3 * r + k];
-
-  // attention work list: longest sequences first
-  AttnWork work;
-  std::memset(&work, 0, sizeof(work));
-  work.n = n_seqs;
-  for (int r = 0; r <= n_seqs; ++r) work.cu[r] = cu_seqlens[r];
-  std::vector<int> ord(n_seqs);
-  for (int r = 0; r < n_seqs; ++r) ord[r] = r;
-  std::stable_sort(ord.begin(), ord.end(), [&](int a, int b) {
-    return cu_seqlens[a + 1] - cu_seqlens[a] > cu_seqlens[b + 1] - cu_seqlens[b];
-  });
-  // queries per work-list tile of the attention kernel that will run
-  AttnArgs probe;
-  std::memset(&probe, 0, sizeof(probe));
-  probe.qkv = enc->qkv;
-  probe.ldqkv = 3 * d;
-  probe.hd = hd;
-  const int qt = bf && attention_dma_supported(probe, N) ? attention_dma_q_tile(hd) : attention_q_tile(bf);
-  int tiles = 0;
-  double attn_flops = 0.0;
-  for (int i = 0; i < n_seqs; ++i) {
-    const int r = ord[i];
-    const int L = cu_seqlens[r + 1] - cu_seqlens[r];
-    work.order[i] = r;
-    work.tile_start[i] = tiles;
-    tiles += (L + qt - 1) / qt;
-    attn_flops += 4.0 * (double)L * L * hd * H;
-  }
-  work.tile_start[n_seqs] = tiles;
-
-  auto W = [&](const std::string& n) { return wptr(weights, enc, n); };
   eas_status rc = EAS_OK;
-#define EAS_TRY(expr)          \
-  do {                         \
-    rc = (expr);               \
-    if (rc != EAS_OK) return rc; \
-  } while (0)
-
-  const bool vit = c.kind != EAS_KIND_WHISPER;
-  const bool need_pos = vit;
-  if (need_pos)
-    EAS_TRY(run(enc, s, 0.0, (double)N * 20, [&](const char** kn) {
-      *kn = "positions";
-      return launch_positions(meta, N, enc->pos3, enc->tab_idx, c.pos_grid[1], s);
-    }));
-
-  // ---- embedding ----
-  if (vit) {
-    const int K = (int)k_patch(c);
-    GemmArgs g = gemm_args(N, d, K, packed_in, K, W("patch.w"), K, enc->x, d, 1);
-    if (enc->kpad) {   // zero-padded copies: the patch GEMM runs whole 64-wide k-tiles
-      const int kp = enc->kpad;
-      EAS_TRY(run(enc, s, 0.0, (double)N * (K + kp) * 2, [&](const char** kn) {
-        *kn = "pad_cols";
-        return launch_pad_cols16(packed_in, N, K, kp, enc->hbuf, s);
-      }));
-      EAS_TRY(run(enc, s, 0.0, (double)d * (K + kp) * 2, [&](const char** kn) {
-        *kn = "pad_cols";
-        return launch_pad_cols16(W("patch.w"), d, K, kp, enc->patch_w, s);
-      }));
-      g = gemm_args(N, d, kp, enc->hbuf, kp, enc->patch_w, kp, enc->x, d, 1);
-    }
-    g.bias = W("patch.b");
-    if (c.kind != EAS_KIND_VIT_ROPE) {
-      g.pos = W("pos");
-      g.pos_f32 = !bf;
-      g.ld_pos = d;
-      g.pos_idx = enc->tab_idx;
-    }
-    EAS_TRY(gemm(enc, g, s));
-    if (c.kind == EAS_KIND_VIT_CLS_ABS) {
-      EAS_TRY(run(enc, s, 0.0, (double)n_seqs * d * 4, [&](const char** kn) {
-        *kn = "cls_insert";
-        return launch_cls(meta, enc->x, d, W("cls"), W("pos"), bf, s);
-      }));
-      EAS_TRY(run(enc, s, 0.0, (double)N * d * 8, [&](const char** kn) {
-        *kn = "ln_apply";
-        return launch_ln_apply(enc->x, N, d, c.ln_eps, W("ln_pre.g"), W("ln_pre.b"), bf, enc->x, 1, s);
-      }));
-    }
+  if (enc->kpad) {   // the zero-padded patch weight, shared by both halves of a split call
+    const int K = (int)k_patch(c), kp = enc->kpad, d = c.hidden;
+    rc = run(enc, s, 0.0, (double)d * (K + kp) * 2, [&](const char** kn) {
+      *kn = "pad_cols";
+      return launch_pad_cols16(wptr(weights, enc, "patch.w"), d, K, kp, enc->patch_w, s);
+    });
+    if (rc != EAS_OK) return rc;
+  }
+  int64_t in_off = 0, out_off = 0;
+  const int k = split_point(enc, cu_seqlens, n_seqs, &in_off, &out_off);
+  if (k == 0) {
+    rc = encode_part(enc, enc->rows_from(0), packed_in, cu_seqlens, grid_thw, n_seqs, weights, out_embeddings, s);
   } else {
-    const int nc = n_seqs, F = c.n_frames, C = c.n_mels;
-    // conv1: im2col [nc*F, 3C] (in ao) -> GEMM + GELU -> [nc*F, d] (in qkv)
-    EAS_TRY(run(enc, s, 0.0, (double)nc * F * C * 3 * el * 2, [&](const char** kn) {
-      *kn = "im2col_k3";
-      return launch_im2col_k3(packed_in, F, C, nc, 1, bf, enc->ao, s);
-    }));
-    GemmArgs g1 = gemm_args(nc * F, d, 3 * C, enc->ao, 3 * C, W("conv1.w"), 3 * C, enc->qkv, d, 0);
-    if (!bf) g1.out_f32 = 1;
-    g1.bias = W("conv1.b");
-    g1.act = ACT_GELU;
-    EAS_TRY(gemm(enc, g1, s));
-    // conv2 (stride 2): im2col [nc*F/2, 3d] (in hbuf) -> GEMM + GELU + sinusoid -> x
-    EAS_TRY(run(enc, s, 0.0, (double)nc * (F / 2) * d * 3 * el * 2, [&](const char** kn) {
-      *kn = "im2col_k3";
-      return launch_im2col_k3(enc->qkv, F, d, nc, 2, bf, enc->hbuf, s);
-    }));
-    GemmArgs g2 = gemm_args(N, d, 3 * d, enc->hbuf, 3 * d, W("conv2.w"), 3 * d, enc->x, d, 1);
-    g2.bias = W("conv2.b");
-    g2.act = ACT_GELU;
-    g2.pos = enc->sinus;
-    g2.pos_f32 = 1;
-    g2.ld_pos = d;
-    g2.pos_period = F / 2;
-    EAS_TRY(gemm(enc, g2, s));
+    // requests [0, k) on the caller's stream and [k, n) on the encoder's second
+    // stream, forked from the caller's stream and joined back into it
+    std::vector<int32_t> cub(n_seqs - k + 1);
+    for (int r = 0; r <= n_seqs - k; ++r) cub[r] = cu_seqlens[k + r] - cu_seqlens[k];
+    if (hipEventRecord(enc->ev_fork, s) != hipSuccess || hipStreamWaitEvent(enc->side, enc->ev_fork, 0) != hipSuccess)
+      return fail(enc, EAS_ERR_HIP, "stream fork failed");
+    rc = encode_part(enc, enc->rows_from(0), packed_in, cu_seqlens, grid_thw, k, weights, out_embeddings, s);
+    if (rc == EAS_OK)
+      rc = encode_part(enc, enc->rows_from(cu_seqlens[k]), static_cast<const char*>(packed_in) + in_off, cub.data(),
+                       grid_thw ? grid_thw + 3 * k : nullptr, n_seqs - k, weights,
+                       static_cast<char*>(out_embeddings) + out_off, enc->side);
+    // joined even after an error: the caller's stream never runs ahead of the side stream
+    const bool joined = hipEventRecord(enc->ev_join, enc->side) == hipSuccess &&
+                        hipStreamWaitEvent(s, enc->ev_join, 0) == hipSuccess;
+    if (rc == EAS_OK && !joined) rc = fail(enc, EAS_ERR_HIP, "stream join failed");
   }
-
-  // ---- layers ----
-  const int act = c.act == EAS_ACT_GELU ? ACT_GELU : ACT_QUICKGELU;
-  const int mid_f32 = bf ? 0 : 1;   // qkv / attention / MLP activations: model dtype
-  for (int l = 0; l < c.layers; ++l) {
-    const std::string p = "layers." + std::to_string(l) + ".";
-    GemmArgs gq = gemm_args(N, d3, d, enc->x, d, W(p + "qkv.w"), d, enc->qkv, d3, mid_f32);
-    gq.ln_g = W(p + "ln1.g");
-    gq.ln_b = W(p + "ln1.b");
-    gq.ln_dim = d;
-    gq.bias = W(p + "qkv.b");
-    EAS_TRY(ln_gemm(enc, gq, c.ln_eps, 1, s));
-    if (c.kind == EAS_KIND_VIT_ROPE)
-      EAS_TRY(run(enc, s, 0.0, (double)N * 2 * d * el * 2 + (double)N * 16, [&](const char** kn) {
-        *kn = "rope";
-        return launch_rope(enc->qkv, d3, N, H, hd, bf, enc->pos3, enc->inv_freq, enc->slot_axis, s);
-      }));
-    AttnArgs aa;
-    aa.qkv = enc->qkv;
-    aa.ldqkv = d3;
-    aa.out = enc->ao;
-    aa.ldo = d;
-    aa.heads = H;
-    aa.hd = hd;
-    aa.scale = (float)(1.0 / std::sqrt((double)hd));
-    EAS_TRY(run(enc, s, attn_flops, (double)N * 4 * d * el, [&](const char** kn) {
-      return bf ? launch_attention_bf16(aa, work, tiles, N, s, kn) : launch_attention_f32(aa, work, tiles, s, kn);
-    }));
-    GemmArgs go = gemm_args(N, d, d, enc->ao, d, W(p + "o.w"), d, enc->x, d, 1);
-    go.bias = W(p + "o.b");
-    go.resid = enc->x;
-    go.ldr = d;
-    EAS_TRY(gemm(enc, go, s));
-    GemmArgs g1 = gemm_args(N, f, d, enc->x, d, W(p + "fc1.w"), d, enc->hbuf, f, mid_f32);
-    g1.ln_g = W(p + "ln2.g");
-    g1.ln_b = W(p + "ln2.b");
-    g1.ln_dim = d;
-    g1.bias = W(p + "fc1.b");
-    g1.act = act;
-    EAS_TRY(ln_gemm(enc, g1, c.ln_eps, 1, s));
-    // the CLS model's output is the final residual stream: the last FC2 writes it directly
-    const bool direct = c.kind == EAS_KIND_VIT_CLS_ABS && l == c.layers - 1;
-    GemmArgs g2 = gemm_args(N, d, f, enc->hbuf, f, W(p + "fc2.w"), f, direct ? out_embeddings : (void*)enc->x, d,
-                            direct ? out_f32 : 1);
-    g2.bias = W(p + "fc2.b");
-    g2.resid = enc->x;
-    g2.ldr = d;
-    EAS_TRY(gemm(enc, g2, s));
-  }
-
-  // ---- connector ----
-  if (c.merge == 2) {
-    const int G = N / 4, d4 = 4 * d;
-    GemmArgs m1 = gemm_args(G, d4, d4, enc->x, d4, W("m1.w"), d4, enc->hbuf, d4, mid_f32);
-    m1.ln_g = W("ln_q.g");
-    m1.ln_b = W("ln_q.b");
-    m1.ln_dim = d;
-    m1.bias = W("m1.b");
-    m1.act = ACT_GELU;
-    EAS_TRY(ln_gemm(enc, m1, c.merger_ln_eps, 4, s));
-    GemmArgs m2 = gemm_args(G, c.out_dim, d4, enc->hbuf, d4, W("m2.w"), d4, out_embeddings, c.out_dim, out_f32);
-    m2.bias = W("m2.b");
-    EAS_TRY(gemm(enc, m2, s));
-  } else if (c.kind == EAS_KIND_WHISPER) {
-    EAS_TRY(run(enc, s, 0.0, (double)N * d * (4 + (out_f32 ? 4 : 2)), [&](const char** kn) {
-      *kn = "ln_apply";
-      return launch_ln_apply(enc->x, N, d, c.ln_eps, W("ln_post.g"), W("ln_post.b"), bf, out_embeddings, out_f32, s);
-    }));
-  } else if (c.layers == 0) {   // CLS model without layers: the embedding is the output
-    if (hipMemcpyAsync(out_embeddings, enc->x, (size_t)N * d * 4, hipMemcpyDeviceToDevice, s) != hipSuccess)
-      return fail(enc, EAS_ERR_HIP, "hipMemcpyAsync failed");
-  }
-#undef EAS_TRY
+  if (rc != EAS_OK) return rc;
   if (cu_out) {
     for (int r = 0; r <= n_seqs; ++r) cu_out[r] = c.merge == 2 ? cu_seqlens[r] / 4 : cu_seqlens[r];
   }
