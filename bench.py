@@ -213,6 +213,7 @@ def kernel_table(prof, passes):
     """Per-kernel time per pass, share, and TFLOP/s (MFMA kernels) or GB/s."""
     total_ms = sum(v["ms"] for v in prof.values())
     return {k: {"ms_per_step": v["ms"] / passes, "share": v["ms"] / total_ms,
+                "launches_per_step": v["launches"] / passes,
                 "tflops" if k.startswith(MFMA_KERNELS) else "gbs":
                     (v["flops"] / (v["ms"] * 1e-3) / 1e12) if k.startswith(MFMA_KERNELS)
                     else (v["bytes"] / (v["ms"] * 1e-3) / 1e9)}
