@@ -578,22 +578,34 @@ eas_status encode_part(eas_encoder* enc, const Workspace& ws, const void* packed
 // and [k, n) split about evenly by tokens: each half's kernels fill the other's
 // partial GEMM rounds and overlap its memory-bound steps.  A request's result
 // does not depend on the split (every kernel choice gives the same bits).
-// Returns k, or 0 for one pass: per-kernel profiling (one stream of events),
-// small batches, and halves whose buffers would lose 16-byte alignment.
+// The boundary is the first one at or past half the tokens, else the nearest
+// within two requests of it whose second-half buffers keep 16-byte alignment
+// (CLIP's 588-element patch rows need an even token offset).  Returns k, or 0
+// for one pass: per-kernel profiling (one stream of events), small batches,
+// and no aligned boundary near the middle.
 constexpr int kSplitTokens = 16384;
 int split_point(const eas_encoder* e, const int32_t* cu, int n, int64_t* in_off, int64_t* out_off) {
   const eas_config& c = e->cfg;
   if (e->prof || !e->side || n < 2 || cu[n] < kSplitTokens) return 0;
-  int k = 1;
-  while (k < n - 1 && 2 * (int64_t)cu[k] < cu[n]) ++k;
-  const int64_t el = c.dtype == EAS_BF16 ? 2 : 4, oel = c.out_dtype == EAS_FP32 ? 4 : 2, r0 = cu[k];
-  *in_off = c.kind == EAS_KIND_WHISPER ? (int64_t)k * c.n_mels * c.n_frames * el : r0 * k_patch(c) * el;
-  *out_off = (c.merge == 2 ? r0 / 4 : r0) * c.out_dim * oel;
-  const int64_t offs[] = {*in_off, *out_off, r0 * c.hidden * 4, r0 * 3 * c.hidden * el, r0 * e->ao_w * el,
-                          r0 * e->hw * el, r0 * c.hidden * el};
-  for (int64_t o : offs)
-    if (o % 16) return 0;
-  return k;
+  int k0 = 1;
+  while (k0 < n - 1 && 2 * (int64_t)cu[k0] < cu[n]) ++k0;
+  const int64_t el = c.dtype == EAS_BF16 ? 2 : 4, oel = c.out_dtype == EAS_FP32 ? 4 : 2;
+  for (int k : {k0, k0 - 1, k0 + 1, k0 - 2, k0 + 2}) {
+    if (k < 1 || k > n - 1) continue;
+    const int64_t r0 = cu[k];
+    const int64_t in = c.kind == EAS_KIND_WHISPER ? (int64_t)k * c.n_mels * c.n_frames * el : r0 * k_patch(c) * el;
+    const int64_t out = (c.merge == 2 ? r0 / 4 : r0) * c.out_dim * oel;
+    const int64_t offs[] = {in, out, r0 * c.hidden * 4, r0 * 3 * c.hidden * el, r0 * e->ao_w * el,
+                            r0 * e->hw * el, r0 * c.hidden * el};
+    bool ok = true;
+    for (int64_t o : offs) ok = ok && o % 16 == 0;
+    if (ok) {
+      *in_off = in;
+      *out_off = out;
+      return k;
+    }
+  }
+  return 0;
 }
 
 }  // namespace

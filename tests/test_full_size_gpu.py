@@ -5,10 +5,11 @@ Each test encodes a whole benchmarked micro-batch (the same seeded request
 pools as bench.py) and checks sampled requests against the fp64 reference run
 on that request alone, at full depth where the reference finishes in seconds
 and at two layers otherwise; it also checks that each sampled request's rows
-are bit-identical to its own micro-batch-1 encoding.  At these sizes the
-GEMMs run the large-tile path, including the split of quantised grids into a
-256 x 256 head launch and a 128 x 128 tail launch, and attention runs over the
-longest sequences (9216-token images, 8192-token clips).
+are bit-identical to its own micro-batch-1 encoding.  At these sizes each
+micro-batch runs as two concurrent halves on two streams, the GEMMs run the
+large-tile path, including the split of quantised grids into a 256 x 256 head
+launch and a smaller-tile tail launch, and attention runs over the longest
+sequences (9216-token images, 8192-token clips).
 """
 import numpy as np
 import pytest

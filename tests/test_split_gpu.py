@@ -1,0 +1,49 @@
+"""Micro-batches of 16384 tokens or more run as two concurrent halves, split at a
+request boundary near half the tokens (the second half on the handle's own
+stream).  Every request of such a batch must come out bit-identical to its own
+micro-batch-1 encoding (which runs in one pass), and match the fp64 reference.
+
+The cases put the boundary where the split logic has choices to make: CLIP with
+29 images (the balanced boundary, after 15 images, would leave the second
+half's patch rows off 16-byte alignment, so the split moves to 14), Qwen images
+with a 256-token second half against 18432 tokens in the first, Whisper with an
+odd clip count, and video at exactly the 16384-token threshold.
+"""
+import numpy as np
+import pytest
+
+from _harness import TOL, gpu_encode, oracle_encode, rel_err
+from paper_2609_31551_amd import configs as C
+from paper_2609_31551_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+# preset, items (count, or explicit shapes), requests checked against the reference
+CASES = {
+    "clip_29": (C.CLIP_L336, 29, None, [0, 14, 28]),
+    "qwen_uneven": (C.QWEN_IMAGE, 3, [(2, 1344, 1344), (2, 1344, 1344), (2, 224, 224)], [2]),
+    "whisper_11": (C.WHISPER_L, 11, None, [0, 6, 10]),
+    "video_threshold": (C.QWEN_VIDEO, 2, None, []),
+}
+
+
+@pytest.mark.parametrize("case", list(CASES))
+def test_split_batch_matches_single_requests_and_reference(case):
+    base, n, shapes, checked = CASES[case]
+    p = C.with_layers(base, 2)
+    W = synth.make_weights(p, 0)
+    items = synth.make_items(p, n, 0, shapes=shapes)
+    batch = gpu_encode(p, items, W)
+    assert batch["cu"][-1] >= 16384, batch["cu"][-1]
+    enc, wdev, cu = batch["enc"], batch["wdev"], batch["cu_out"]
+    for r in range(n):
+        print("[split] %s: request %d of %d alone" % (case, r, n), flush=True)
+        alone = gpu_encode(p, [items[r]], W, enc=enc, wdev=wdev)
+        np.testing.assert_array_equal(alone["out"], batch["out"][cu[r]:cu[r + 1]])
+    for r in checked:
+        ref = oracle_encode(p, [items[r]], W)
+        e = rel_err(batch["out"][cu[r]:cu[r + 1]], ref["out"])
+        print("[split] %s: request %d relative error %.3g" % (case, r, e), flush=True)
+        assert e <= TOL[p["dtype"]], (r, e)
+    again = gpu_encode(p, items, W, enc=enc, wdev=wdev)
+    np.testing.assert_array_equal(again["out"], batch["out"])
