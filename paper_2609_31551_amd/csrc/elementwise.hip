@@ -169,51 +169,61 @@ __global__ void rope_kernel(T* qkv, int ldqkv, int N, int heads, int hd, const i
   }
 }
 
-// bf16 form: one thread per (token, 8 consecutive slots); the 8 angles are
-// computed once and applied to every head of q and of k with 16-byte
-// accesses (hd % 16 == 0).
-__global__ void rope_vec_kernel(bf16* qkv, int ldqkv, int N, int heads, int hd, const int4* pos3,
-                                const float* inv_freq, const int* slot_axis) {
+// bf16 RoPE, one block per ROPE_TOK tokens: the (cos, sin) of every rotation
+// slot of its tokens are computed once into LDS, then the block's threads
+// rotate the (x_k, x_{k+half}) 16-byte chunk pairs of q and k, consecutive
+// threads on consecutive chunks (a row's q and k heads are one contiguous
+// stretch of 2 * heads * hd elements), ROPE_R pairs per thread with all their
+// loads issued before the first store.  hd % 16 == 0, hd <= 128.
+constexpr int ROPE_TOK = 8, ROPE_R = 5;
+__global__ __launch_bounds__(256) void rope_vec_kernel(bf16* qkv, int ldqkv, int N, int heads, int hd,
+                                                       const int4* pos3, const float* inv_freq, const int* slot_axis) {
+  __shared__ float2 tab[ROPE_TOK * 64];   // [token][slot]: (cos, sin)
   const int half = hd >> 1, chunks = half >> 3;
-  const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= (long)N * chunks) return;
-  const int i = (int)(idx / chunks), k0 = (int)(idx % chunks) * 8;
-  const int4 p = pos3[i];
-  float sn[8], cs[8];
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const int ax = slot_axis[k0 + j];
+  const int t0 = blockIdx.x * ROPE_TOK, nt = min(ROPE_TOK, N - t0);
+  for (int e = threadIdx.x; e < nt * half; e += blockDim.x) {
+    const int t = e / half, k = e % half;
+    const int4 p = pos3[t0 + t];
+    const int ax = slot_axis[k];
     const float pos = (float)(ax == 0 ? p.x : (ax == 1 ? p.y : p.z));
-    sincosf(pos * inv_freq[k0 + j], &sn[j], &cs[j]);
+    float sn, cs;
+    sincosf(pos * inv_freq[k], &sn, &cs);
+    tab[t * 64 + k] = make_float2(cs, sn);
   }
-  // head-parts of q (0 .. heads-1) then k (heads .. 2 heads-1), four at a time:
-  // all loads of a group are issued before its stores, so a thread keeps eight
-  // 16-byte loads in flight instead of waiting out one round trip per head
-  constexpr int G = 4;
-  bf16* row = qkv + (long)i * ldqkv + k0;
-  for (int h0 = 0; h0 < 2 * heads; h0 += G) {
-    union { uint4 u; bf16 e[8]; } a[G], c[G];
+  __syncthreads();
+  const int per_tok = 2 * heads * chunks;   // chunk pairs of q and k per token
+  const int items = nt * per_tok;
+  for (int i0 = 0; i0 < items; i0 += ROPE_R * 256) {
+    union { uint4 u; bf16 e[8]; } a[ROPE_R], c[ROPE_R];
+    bf16* ptr[ROPE_R];
+    int ti[ROPE_R], kk[ROPE_R];
 #pragma unroll
-    for (int u = 0; u < G; ++u) {
-      if (h0 + u < 2 * heads) {
-        const bf16* base = row + (h0 + u >= heads ? heads * hd : 0) + ((h0 + u) % heads) * hd;
-        a[u].u = *reinterpret_cast<const uint4*>(base);
-        c[u].u = *reinterpret_cast<const uint4*>(base + half);
+    for (int r = 0; r < ROPE_R; ++r) {
+      const int it = i0 + r * 256 + (int)threadIdx.x;
+      ptr[r] = nullptr;
+      if (it < items) {
+        const int t = it / per_tok, w = it % per_tok;
+        ti[r] = t;
+        kk[r] = (w % chunks) * 8;
+        ptr[r] = qkv + (long)(t0 + t) * ldqkv + (w / chunks) * hd + kk[r];
+        a[r].u = *reinterpret_cast<const uint4*>(ptr[r]);
+        c[r].u = *reinterpret_cast<const uint4*>(ptr[r] + half);
       }
     }
 #pragma unroll
-    for (int u = 0; u < G; ++u) {
-      if (h0 + u < 2 * heads) {
-        bf16* base = row + (h0 + u >= heads ? heads * hd : 0) + ((h0 + u) % heads) * hd;
+    for (int r = 0; r < ROPE_R; ++r) {
+      if (ptr[r]) {
+        const float2* f = tab + ti[r] * 64 + kk[r];
         union { uint4 u; bf16 e[8]; } oa, oc;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-          const float x1 = (float)a[u].e[j], x2 = (float)c[u].e[j];
-          oa.e[j] = (bf16)(x1 * cs[j] - x2 * sn[j]);
-          oc.e[j] = (bf16)(x2 * cs[j] + x1 * sn[j]);
+          const float2 q = f[j];
+          const float x1 = (float)a[r].e[j], x2 = (float)c[r].e[j];
+          oa.e[j] = (bf16)(x1 * q.x - x2 * q.y);
+          oc.e[j] = (bf16)(x2 * q.x + x1 * q.y);
         }
-        *reinterpret_cast<uint4*>(base) = oa.u;
-        *reinterpret_cast<uint4*>(base + half) = oc.u;
+        *reinterpret_cast<uint4*>(ptr[r]) = oa.u;
+        *reinterpret_cast<uint4*>(ptr[r] + half) = oc.u;
       }
     }
   }
@@ -333,10 +343,10 @@ hipError_t launch_ln_apply(const float* x, int N, int d, float eps, const void* 
 hipError_t launch_rope(void* qkv, int ldqkv, int N, int heads, int hd, int is_bf16, const int4* pos3,
                        const float* inv_freq, const int* slot_axis, hipStream_t s) {
   const long total = (long)N * heads * (hd / 2);
-  if (is_bf16 && hd % 16 == 0 && ldqkv % 8 == 0 && (uintptr_t)qkv % 16 == 0) {
-    const long threads = (long)N * (hd / 16);
-    hipLaunchKernelGGL(rope_vec_kernel, dim3(blocks_for(threads, 256)), dim3(256), 0, s, (bf16*)qkv, ldqkv, N, heads,
-                       hd, pos3, inv_freq, slot_axis);
+  if (is_bf16 && hd % 16 == 0 && hd <= 128 && ldqkv % 8 == 0 && (uintptr_t)qkv % 16 == 0) {
+    if (N == 0) return hipSuccess;
+    hipLaunchKernelGGL(rope_vec_kernel, dim3((N + ROPE_TOK - 1) / ROPE_TOK), dim3(256), 0, s, (bf16*)qkv, ldqkv, N,
+                       heads, hd, pos3, inv_freq, slot_axis);
     return hipGetLastError();
   }
   if (is_bf16)
