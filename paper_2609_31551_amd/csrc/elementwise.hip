@@ -274,6 +274,68 @@ __global__ void pack_vision_kernel(PackArgs p, int cls, int merge, int patch, in
   out[idx] = (T)p.src[r][src];
 }
 
+// bf16 packer: one thread per (token, c, tau, dy) line of `patch` consecutive
+// pixels, a token's lines on consecutive threads, so its packed row leaves
+// contiguously; pixels are read as float2 pairs and the bf16 values written in
+// pairs (patch and every image width even, 8-byte aligned sources).
+__global__ void pack_vision_vec_kernel(PackArgs p, int cls, int merge, int patch, int tp, int K, int lines, long total,
+                                       bf16* out) {
+  const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= total) return;
+  const int row = (int)(idx / lines), ln = (int)(idx % lines);
+  const int dy = ln % patch, tau = (ln / patch) % tp, c = ln / (patch * tp);
+  unsigned* dst = reinterpret_cast<unsigned*>(out + (long)row * K + (long)ln * patch);
+  const int r = find_seq(p.cu, p.n, row);
+  int j = row - p.cu[r];
+  if (cls) {
+    if (j == 0) {
+      for (int x = 0; x < patch / 2; ++x) dst[x] = 0u;
+      return;
+    }
+    j -= 1;
+  }
+  const int H = p.tchw[r][2], W = p.tchw[r][3], C = p.tchw[r][1];
+  int ti, hi, wi;
+  decode_token(j, H / patch, W / patch, merge, &ti, &hi, &wi);
+  const float2* src = reinterpret_cast<const float2*>(
+      p.src[r] + (((long)(ti * tp + tau) * C + c) * H + hi * patch + dy) * W + wi * patch);
+  for (int x = 0; x < patch / 2; ++x) {
+    const float2 v = src[x];
+    union { unsigned u; bf16 h[2]; } o;
+    o.h[0] = (bf16)v.x;
+    o.h[1] = (bf16)v.y;
+    dst[x] = o.u;
+  }
+}
+
+// bf16 im2col for C % 8 == 0: one thread per (output frame, 8 channels) reads
+// the three taps' 16-byte chunks and writes the 24 values ((channel, tap)
+// order) as three 16-byte stores.
+__global__ void im2col_k3_vec_kernel(const bf16* src, int fin, int C, int fout, int stride, long total, bf16* dst) {
+  const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= total) return;
+  const int cg = C >> 3;
+  const long row = idx / cg;
+  const int c0 = (int)(idx % cg) * 8;
+  const int t = (int)(row % fout);
+  const long clip = row / fout;
+  union { uint4 u; bf16 e[8]; } in[3];
+#pragma unroll
+  for (int k = 0; k < 3; ++k) {
+    const int ts = stride * t + k - 1;
+    in[k].u = (ts >= 0 && ts < fin) ? *reinterpret_cast<const uint4*>(src + (clip * fin + ts) * C + c0)
+                                    : make_uint4(0u, 0u, 0u, 0u);
+  }
+  union { uint4 u[3]; bf16 e[24]; } o;
+#pragma unroll
+  for (int cc = 0; cc < 8; ++cc)
+#pragma unroll
+    for (int k = 0; k < 3; ++k) o.e[cc * 3 + k] = in[k].e[cc];
+  uint4* d = reinterpret_cast<uint4*>(dst + row * 3 * C + c0 * 3);
+#pragma unroll
+  for (int q = 0; q < 3; ++q) d[q] = o.u[q];
+}
+
 // [n_mels, n_frames] -> [n_frames, n_mels] per clip.
 template <class T>
 __global__ void pack_audio_kernel(PackArgs p, int n_mels, int n_frames, T* out) {
@@ -378,6 +440,13 @@ hipError_t launch_im2col_k3(const void* src, int frames_in, int C, int n_clips, 
                             hipStream_t s) {
   const int fout = (frames_in - 1) / stride + 1;
   const long total = (long)n_clips * fout * C * 3;
+  if (total == 0) return hipSuccess;
+  if (is_bf16 && C % 8 == 0 && (uintptr_t)src % 16 == 0 && (uintptr_t)dst % 16 == 0) {
+    const long threads = (long)n_clips * fout * (C / 8);
+    hipLaunchKernelGGL(im2col_k3_vec_kernel, dim3(blocks_for(threads, 256)), dim3(256), 0, s, (const bf16*)src,
+                       frames_in, C, fout, stride, threads, (bf16*)dst);
+    return hipGetLastError();
+  }
   if (is_bf16)
     hipLaunchKernelGGL((im2col_k3_kernel<bf16>), dim3(blocks_for(total, 256)), dim3(256), 0, s, (const bf16*)src,
                        frames_in, C, fout, stride, total, (bf16*)dst);
@@ -389,6 +458,16 @@ hipError_t launch_im2col_k3(const void* src, int frames_in, int C, int n_clips, 
 
 hipError_t launch_pack_vision(const PackArgs& p, int cls, int merge, int patch, int tp, int K, int is_bf16,
                               void* packed, long total, hipStream_t s) {
+  if (total == 0) return hipSuccess;
+  bool vec = is_bf16 && patch % 2 == 0 && (uintptr_t)packed % 4 == 0;
+  for (int r = 0; vec && r < p.n; ++r) vec = p.tchw[r][3] % 2 == 0 && (uintptr_t)p.src[r] % 8 == 0;
+  if (vec) {
+    const int lines = K / patch;
+    const long threads = total / K * lines;
+    hipLaunchKernelGGL(pack_vision_vec_kernel, dim3(blocks_for(threads, 256)), dim3(256), 0, s, p, cls, merge, patch,
+                       tp, K, lines, threads, (bf16*)packed);
+    return hipGetLastError();
+  }
   if (is_bf16)
     hipLaunchKernelGGL((pack_vision_kernel<bf16>), dim3(blocks_for(total, 256)), dim3(256), 0, s, p, cls, merge, patch,
                        tp, K, total, (bf16*)packed);
