@@ -84,17 +84,20 @@ TRAFFIC_SOURCES = {
     "gemm_bf16_64x64": ("gemm_bf16.hip", "common.h", "eas_api.cpp"),
     "gemm_bf16_64x128": ("gemm_bf16.hip", "common.h", "eas_api.cpp"),
     "attn_bf16_hd64": ("attention_dma.hip", "common.h", "eas_api.cpp"),
+    "attn_bf16_hd80": ("attention_dma.hip", "common.h", "eas_api.cpp"),
     "ln_apply_bf16": ("elementwise.hip", "common.h", "eas_api.cpp"),
+    "rope": ("elementwise.hip", "common.h", "eas_api.cpp"),
 }
 
 
-def traffic_record(kernel):
-    """HBM bytes per launch from the committed counter summary, if it was
-    taken on the current sources of that kernel."""
+def traffic_record(workload, kernel):
+    """HBM bytes per launch of `kernel` on `workload` (a preset name and
+    micro-batch size, "clip_vit_l14_336/64") from the committed counter
+    summary, if it was taken on the current sources of that kernel."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path) or kernel not in TRAFFIC_SOURCES:
         return None
-    rec = json.load(open(path)).get(kernel)
+    rec = json.load(open(path)).get(workload, {}).get(kernel)
     if not rec:
         return None
     if rec.get("source_sha") != source_sha(TRAFFIC_SOURCES[kernel]):
@@ -455,7 +458,8 @@ def main():
             peak, unit = PEAK_HBM_GBS, "GB/s"
         result["roofline"] = {"bound": "mfma" if is_mfma else "hbm", "kernel": dom, "achieved": achieved,
                               "peak": peak, "unit": unit, "frac": achieved / peak,
-                              "traffic": traffic_record(dom), "traffic_unit": "HBM bytes per launch",
+                              "traffic": traffic_record("%s/%d" % (args.preset, args.batch), dom),
+                              "traffic_unit": "HBM bytes per launch",
                               "mean_launch_ms": per_launch_ms,
                               "launches_per_step": p["launches"] / args.steps}
         result["kernels"] = kernel_table(prof, args.steps)
