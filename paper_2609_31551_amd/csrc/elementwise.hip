@@ -274,38 +274,46 @@ __global__ void pack_vision_kernel(PackArgs p, int cls, int merge, int patch, in
   out[idx] = (T)p.src[r][src];
 }
 
-// bf16 packer: one thread per (token, c, tau, dy) line of `patch` consecutive
-// pixels, a token's lines on consecutive threads, so its packed row leaves
-// contiguously; pixels are read as float2 pairs and the bf16 values written in
-// pairs (patch and every image width even, 8-byte aligned sources).
-__global__ void pack_vision_vec_kernel(PackArgs p, int cls, int merge, int patch, int tp, int K, int lines, long total,
-                                       bf16* out) {
-  const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= total) return;
-  const int row = (int)(idx / lines), ln = (int)(idx % lines);
-  const int dy = ln % patch, tau = (ln / patch) % tp, c = ln / (patch * tp);
-  unsigned* dst = reinterpret_cast<unsigned*>(out + (long)row * K + (long)ln * patch);
-  const int r = find_seq(p.cu, p.n, row);
-  int j = row - p.cu[r];
-  if (cls) {
-    if (j == 0) {
+// bf16 packer: a block packs `tpb` consecutive token rows.  One thread per
+// (token, c, tau, dy) line of `patch` pixels reads them as float2 pairs and
+// writes the bf16 values into the block's LDS copy of the rows; the block then
+// stores the rows' contiguous span with 8-byte writes, so every output line is
+// written whole (patch even, every image width even, 8-byte aligned sources,
+// lines <= 256, patch <= 16).
+__global__ __launch_bounds__(256) void pack_vision_vec_kernel(PackArgs p, int cls, int merge, int patch, int tp, int K,
+                                                              int lines, int tpb, int rows, bf16* out) {
+  __shared__ __attribute__((aligned(16))) unsigned buf[256 * 16 / 2];   // tpb * K bf16
+  const int row0 = blockIdx.x * tpb, nrows = min(tpb, rows - row0);
+  const int t = threadIdx.x / lines, ln = threadIdx.x % lines;
+  if (t < nrows) {
+    const int row = row0 + t;
+    unsigned* dst = buf + (t * K + ln * patch) / 2;
+    const int r = find_seq(p.cu, p.n, row);
+    int j = row - p.cu[r];
+    if (cls && j == 0) {
       for (int x = 0; x < patch / 2; ++x) dst[x] = 0u;
-      return;
+    } else {
+      j -= cls;
+      const int dy = ln % patch, tau = (ln / patch) % tp, c = ln / (patch * tp);
+      const int H = p.tchw[r][2], W = p.tchw[r][3], C = p.tchw[r][1];
+      int ti, hi, wi;
+      decode_token(j, H / patch, W / patch, merge, &ti, &hi, &wi);
+      const float2* src = reinterpret_cast<const float2*>(
+          p.src[r] + (((long)(ti * tp + tau) * C + c) * H + hi * patch + dy) * W + wi * patch);
+      for (int x = 0; x < patch / 2; ++x) {
+        const float2 v = src[x];
+        union { unsigned u; bf16 h[2]; } o;
+        o.h[0] = (bf16)v.x;
+        o.h[1] = (bf16)v.y;
+        dst[x] = o.u;
+      }
     }
-    j -= 1;
   }
-  const int H = p.tchw[r][2], W = p.tchw[r][3], C = p.tchw[r][1];
-  int ti, hi, wi;
-  decode_token(j, H / patch, W / patch, merge, &ti, &hi, &wi);
-  const float2* src = reinterpret_cast<const float2*>(
-      p.src[r] + (((long)(ti * tp + tau) * C + c) * H + hi * patch + dy) * W + wi * patch);
-  for (int x = 0; x < patch / 2; ++x) {
-    const float2 v = src[x];
-    union { unsigned u; bf16 h[2]; } o;
-    o.h[0] = (bf16)v.x;
-    o.h[1] = (bf16)v.y;
-    dst[x] = o.u;
-  }
+  __syncthreads();
+  const int n8 = nrows * K / 4;   // 8-byte pieces of the block's rows (K % 4 == 0)
+  uint2* o8 = reinterpret_cast<uint2*>(out + (long)row0 * K);
+  const uint2* b8 = reinterpret_cast<const uint2*>(buf);
+  for (int i = threadIdx.x; i < n8; i += blockDim.x) o8[i] = b8[i];
 }
 
 // bf16 im2col for C % 8 == 0: one thread per (output frame, 8 channels) reads
@@ -459,13 +467,13 @@ hipError_t launch_im2col_k3(const void* src, int frames_in, int C, int n_clips, 
 hipError_t launch_pack_vision(const PackArgs& p, int cls, int merge, int patch, int tp, int K, int is_bf16,
                               void* packed, long total, hipStream_t s) {
   if (total == 0) return hipSuccess;
-  bool vec = is_bf16 && patch % 2 == 0 && (uintptr_t)packed % 4 == 0;
+  const int lines = K / patch;
+  bool vec = is_bf16 && patch % 2 == 0 && patch <= 16 && lines <= 256 && (uintptr_t)packed % 8 == 0;
   for (int r = 0; vec && r < p.n; ++r) vec = p.tchw[r][3] % 2 == 0 && (uintptr_t)p.src[r] % 8 == 0;
   if (vec) {
-    const int lines = K / patch;
-    const long threads = total / K * lines;
-    hipLaunchKernelGGL(pack_vision_vec_kernel, dim3(blocks_for(threads, 256)), dim3(256), 0, s, p, cls, merge, patch,
-                       tp, K, lines, threads, (bf16*)packed);
+    const int rows = (int)(total / K), tpb = 256 / lines;
+    hipLaunchKernelGGL(pack_vision_vec_kernel, dim3((rows + tpb - 1) / tpb), dim3(256), 0, s, p, cls, merge, patch, tp,
+                       K, lines, tpb, rows, (bf16*)packed);
     return hipGetLastError();
   }
   if (is_bf16)
