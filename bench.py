@@ -59,6 +59,9 @@ def parse():
     ap.add_argument("--cpu-budget-s", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="skip the event-timed roofline pass")
+    ap.add_argument("--colocation", default="",
+                    help="micro-batch sizes of a co-location profile of the headline preset: encode latency "
+                         "with 12.5/30/50/70/90%% of the CUs and the smallest-safe-share table ('' to skip)")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="only run a plain device copy of this many MiB (HBM counter calibration)")
     return ap.parse_args()
@@ -294,6 +297,31 @@ def service_times(rows, pool, bound):
     return [0.0] + [float(v) for v in __import__("numpy").interp(range(1, bound + 1), bs, per)]
 
 
+def colocation(wl, sizes, reps=3):
+    """Encode latency of one pack + encode micro-batch against the share of the
+    CUs left to it (Section 3.4, dynamic SM partitioning), and the table of the
+    largest batch size each share sustains within 20% of exclusive access."""
+    from paper_2609_31551_amd import colocate as K
+
+    def run_for(b):
+        def run(stream):
+            wl.stream = stream
+            wl.step(0, b)
+        return run
+    keep = wl.stream
+    log = lambda m: print("[colocation] " + m, file=sys.stderr, flush=True)
+    exclusive, latency = K.profile(run_for, sizes, K.LEVELS, reps, max_s=3.0, log=log)
+    wl.stream = keep
+    table = K.safe_share_table(latency, exclusive)
+    return {"levels": list(K.LEVELS), "micro_batches": list(sizes), "threshold": K.THRESHOLD,
+            "reps": reps, "cus": K.device_cus(),
+            "exclusive_ms": {str(b): exclusive[b] for b in sizes},
+            "latency_ms": {str(lv): {str(b): latency[lv][b] for b in sizes} for lv in K.LEVELS},
+            "largest_safe_batch": {str(lv): table[lv] for lv in K.LEVELS},
+            "share_for_batch": {str(b): K.select_share(table, b) for b in sizes},
+            "mechanism": "CUs held by a reservation kernel (one workgroup per CU) while encode runs on the rest"}
+
+
 def serving(wl, rows, load, live_s, B=64, p=0.6, max_age=1.0):
     """The Poisson-gap micro-batcher (Section 3.2) in front of this encoder.
 
@@ -418,6 +446,11 @@ def parse_workloads(spec):
 
 def main():
     args = parse()
+    if args.colocation:
+        # the co-location profile runs a reservation beside the encoder's two streams: with
+        # HIP's default of 4 hardware queues per process, streams share queues and run in
+        # order, so encode work could sit behind the reservation (set before HIP starts)
+        os.environ["GPU_MAX_HW_QUEUES"] = "16"
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path (requests shard by "
               "micro-batch across independent encoders); run with --gpus 1", file=sys.stderr)
@@ -481,6 +514,11 @@ def main():
     if sweep and args.serving_s >= 0 and max(sweep) == pool and len(sweep) > 1:
         result["serving"] = serving(wl, workloads[preset["name"]]["sweep"], args.serving_load, args.serving_s,
                                     B=pool)
+    if args.colocation:
+        sizes = [int(b) for b in args.colocation.split(",") if b.strip()]
+        if max(sizes) > pool:
+            raise SystemExit("--colocation sizes must not exceed the pool (%d)" % pool)
+        result["colocation"] = colocation(wl, sizes)
     cpu_configs = {}
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(preset, wl, args.batch, args.cpu_budget_s)

@@ -1,0 +1,48 @@
+/*
+ * eas_colocate.h -- C ABI of the compute-unit reservation used to profile
+ * encode under co-location (libeas.so).
+ *
+ * Paper Section 3.4 ("Dynamic SM partitioning"): the encode worker shares its
+ * GPU with a local prefill worker on disjoint SM subsets, re-split every
+ * micro-batch.  Encode latency is profiled at a few SM-allocation levels, and
+ * for each level the largest batch size whose latency stays close to the
+ * exclusive-access latency is recorded; at run time encode takes the smallest
+ * level whose recorded batch size covers the current micro-batch.
+ *
+ * On MI355X the share is taken by occupancy: eas_cu_reserve launches n_cus
+ * workgroups, each of which claims one whole compute unit (all of its LDS and
+ * all of its vector registers), so kernels launched meanwhile run on the other
+ * CUs only.  The workgroups are spread over the XCDs as the dispatcher places
+ * them (round robin).  A held CU does no work.
+ *
+ * Conventions as in eas_encoder.h: every call returns an eas_status, argument
+ * errors are found before anything is enqueued.
+ */
+#ifndef EAS_COLOCATE_H
+#define EAS_COLOCATE_H
+
+#include "eas_encoder.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Holds n_cus compute units (1 <= n_cus <= the device's CU count) from the
+ * moment the kernel enqueued on `stream` (hipStream_t as void*) starts until
+ * *release != 0 or max_seconds (0 < max_seconds <= 60) have passed, whichever
+ * comes first; every workgroup exits by the time limit at the latest.
+ * started: host memory from hipHostMalloc, int32[n_cus], zeroed by the caller;
+ *   workgroup b writes started[b] = 1 once it is resident, so the caller knows
+ *   the share is held when all n_cus entries are 1.
+ * release: host memory from hipHostMalloc, one int32, 0 at launch; the caller
+ *   writes a non-zero value to end the reservation early.
+ * Both stay allocated until the kernel has finished (synchronise `stream`).
+ * Returns EAS_ERR_INVALID_ARG for NULL pointers or out-of-range sizes, and
+ * EAS_ERR_HIP if the launch fails. */
+eas_status eas_cu_reserve(int32_t n_cus, double max_seconds, int32_t* started, const int32_t* release, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif

@@ -109,3 +109,13 @@ def test_every_router_symbol_is_exported():
     for n in names:
         assert hasattr(eas.LIB, n), n
     assert list(router.EXPORTS) == names
+
+
+def test_every_colocation_symbol_is_exported():
+    from paper_2609_31551_amd import colocate
+    text = open(os.path.join(ROOT, "include", "eas_colocate.h")).read()
+    names = sorted(set(re.findall(r"^\s*(?:eas_status|void)\s+(eas_\w+)\s*\(", text, re.M)))
+    assert names == ["eas_cu_reserve"]
+    for n in names:
+        assert hasattr(eas.LIB, n), n
+    assert list(colocate.EXPORTS) == names
