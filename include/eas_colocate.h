@@ -4,10 +4,10 @@
  *
  * Paper Section 3.4 ("Dynamic SM partitioning"): the encode worker shares its
  * GPU with a local prefill worker on disjoint SM subsets, re-split every
- * micro-batch.  Encode latency is profiled at a few SM-allocation levels, and
- * for each level the largest batch size whose latency stays close to the
- * exclusive-access latency is recorded; at run time encode takes the smallest
- * level whose recorded batch size covers the current micro-batch.
+ * micro-batch.  Encode latency is profiled at a few SM-allocation levels; a
+ * level's table entry is the biggest batch size that runs nearly as fast there
+ * as with the whole GPU, and at run time encode takes the smallest level whose
+ * entry covers the current micro-batch.
  *
  * On MI355X the share is taken by occupancy: eas_cu_reserve launches n_cus
  * workgroups, each of which claims one whole compute unit (all of its LDS and

@@ -6,12 +6,12 @@ TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and
 the package) never touches it.
 
 What it computes (paper Section 3.4, dynamic SM partitioning).  Encode latency
-is measured at a few SM-allocation levels for a range of batch sizes.  For each
-level the table records the largest batch size whose latency stays close to
-the latency with the whole GPU -- here within the 20% threshold drawn in the
-paper's latency-versus-allocation figure, the bound itself included.  Given a
-micro-batch of B requests, encode takes the smallest level whose recorded batch
-size is at least B; if no level qualifies, encode keeps the whole GPU (1.0).
+is measured at a few SM-allocation levels for a range of batch sizes.  A level's
+table entry is the biggest measured batch size that runs at most 20% slower at
+that level than on the whole GPU (the threshold drawn in the paper's
+latency-versus-allocation figure, the bound itself included).  Given a
+micro-batch of B requests, encode takes the smallest level whose entry is at
+least B; if no level qualifies, encode keeps the whole GPU (1.0).
 """
 
 
