@@ -37,6 +37,14 @@ extern "C" {
  * release: host memory from hipHostMalloc, one int32, 0 at launch; the caller
  *   writes a non-zero value to end the reservation early.
  * Both stay allocated until the kernel has finished (synchronise `stream`).
+ * Two limits of the occupancy form, found by measurement:
+ *   - HIP maps streams onto a few hardware queues per process (4 by default),
+ *     and streams sharing a queue run in order: work on a stream that shares
+ *     `stream`'s queue waits for the reservation to end.  Keep the streams in
+ *     use fewer than GPU_MAX_HW_QUEUES (set before HIP starts).
+ *   - Leave at least one free CU per shader engine (32 CUs on MI355X): with
+ *     fewer, some shader engine has none, and other kernels stall behind it
+ *     until the reservation ends.
  * Returns EAS_ERR_INVALID_ARG for NULL pointers or out-of-range sizes, and
  * EAS_ERR_HIP if the launch fails. */
 eas_status eas_cu_reserve(int32_t n_cus, double max_seconds, int32_t* started, const int32_t* release, void* stream);
