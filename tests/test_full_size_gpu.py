@@ -53,6 +53,17 @@ def test_qwen_image_microbatch_8_full_depth():
     _check_samples(p, items, W, [int(np.argmin(sizes))])
 
 
+def test_qwen_image_microbatch_32_full_depth():
+    """The largest swept micro-batch of the image workload: the first 32 images
+    of the 64-image pool, full depth; the smallest image is checked against the
+    reference."""
+    p = C.QWEN_IMAGE
+    W = synth.make_weights(p, 0)
+    items = synth.make_items(p, 64, 0)[:32]
+    sizes = [a.shape[2] * a.shape[3] for a in items]
+    _check_samples(p, items, W, [int(np.argmin(sizes))])
+
+
 def test_qwen_image_largest_images_two_layers():
     """Micro-batch with 1344 x 1344 images (9216 tokens each, the longest
     attention rows of the image workload) at two layers."""
