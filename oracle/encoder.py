@@ -26,6 +26,13 @@ transformer encoder:
 
 Everything is float64 and written for a reader to check by eye: numpy's
 matmul is the only library step; nothing is blocked, fused or reordered.
+
+Pins (tests/test_oracle_pins.py): every part is checked against something
+other than itself -- brute-force masked attention, closed forms, torch's
+layer norm, attention, convolutions and pre-LN encoder layer, a normal-CDF
+table for GELU, RoPE identities, and an explicit spatial gather for the merger.
+Parity unpinned: whole-encoder outputs against the paper, which prints no
+encoder outputs to compare with.
 """
 import math
 
