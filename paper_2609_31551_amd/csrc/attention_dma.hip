@@ -85,8 +85,12 @@ __device__ __forceinline__ void decode(const AttnWork& w, int tile, int qt, int*
   *q0 = *s0 + (tile - w.tile_start[i]) * qt;
 }
 
+// head_dim 80 is held to 128 VGPRs (4 waves per SIMD) explicitly: left to
+// itself the register allocator takes 130 and loses a wave per SIMD
 template <int HD, int QB>
-__global__ __launch_bounds__(QTILE / QB * 2) void attn_bf16_dma_kernel(AttnArgs a, AttnWork w) {
+__global__ __launch_bounds__(QTILE / QB * 2)
+__attribute__((amdgpu_waves_per_eu(HD > 64 ? 4 : 1, HD > 64 ? 4 : 8)))
+void attn_bf16_dma_kernel(AttnArgs a, AttnWork w) {
   using C = AttnCfg<HD, QB>;
   extern __shared__ __attribute__((aligned(1024))) char smem[];
   const unsigned lds0 = (unsigned)(size_t)((__attribute__((address_space(3))) char*)smem);
@@ -150,7 +154,7 @@ __global__ __launch_bounds__(QTILE / QB * 2) void attn_bf16_dma_kernel(AttnArgs 
       for (int e = 0; e < 16; ++e) o[qb][hb][e] = 0.0f;
   float m_run[QB], l_part[QB];
 #pragma unroll
-  for (int qb = 0; qb < QB; ++qb) { m_run[qb] = -INFINITY; l_part[qb] = 0.0f; }
+  for (int qb = 0; qb < QB; ++qb) { m_run[qb] = 0.0f; l_part[qb] = 0.0f; }
 
   // K operand reads: row kb*32 + l32, logical chunk 2ks + g (the rotation only
   // depends on row & 7, i.e. on l32)
@@ -220,12 +224,20 @@ __global__ __launch_bounds__(QTILE / QB * 2) void attn_bf16_dma_kernel(AttnArgs 
         }
     };
     // Online softmax.  Scores are masked only in a half that reaches past the
-    // sequence end.  The running max m (log2 units, scale folded in) is raised
-    // lazily: O and the row sum keep a stale m until a lane's max exceeds it
-    // by more than 8, so p = 2^(s*c - m) <= 256 and the rescale of O is
-    // usually skipped; both share m, so O / sum is unchanged.
-    auto softmax = [&](int kb, f32x16* sc, bf16x8 (*pb)[2]) {
+    // sequence end.  One FMA turns each score into x = s*c - m, log2 units
+    // relative to the running max m (scale folded in), and the max is taken
+    // over x.  m is raised lazily: O and the row sum keep a stale m until some
+    // x exceeds 8, so p = 2^x <= 256 and the rescale of O is usually skipped;
+    // both share m, so O / sum is unchanged.  m starts at 0, and the first
+    // half tile (`first`) always sets it to that tile's max.
+    auto softmax = [&](int kb, bool first, f32x16* sc, bf16x8 (*pb)[2]) {
       const int kh = k0 + kb * 32;
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) {
+        const float nm = -m_run[qb];
+#pragma unroll
+        for (int e = 0; e < 16; ++e) sc[qb][e] = fmaf(sc[qb][e], c, nm);
+      }
       if (kh + 32 > s1) {
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb)
@@ -240,25 +252,26 @@ __global__ __launch_bounds__(QTILE / QB * 2) void attn_bf16_dma_kernel(AttnArgs 
         for (int e = 1; e < 16; ++e) mx = fmaxf(mx, sc[qb][e]);
         {   // both 16-key halves of query l % 32: lanes l and l ^ 32, swapped in VALU
           const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
-          mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1])) * c;
+          mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
         }
-        const bool need = mx > m_run[qb] + 8.0f;
+        const bool need = first || mx > 8.0f;
         if (__any(need)) {
-          const float m_new = need ? fmaxf(m_run[qb], mx) : m_run[qb];
-          const float alpha = __builtin_amdgcn_exp2f(m_run[qb] - m_new);
-          m_run[qb] = m_new;
+          const float d = need ? mx : 0.0f;   // m rises by d
+          const float alpha = first ? 0.0f : __builtin_amdgcn_exp2f(-d);   // O and l are still 0 at first
+          m_run[qb] += d;
           l_part[qb] *= alpha;
 #pragma unroll
           for (int hb = 0; hb < C::HB; ++hb)
 #pragma unroll
             for (int e = 0; e < 16; ++e) o[qb][hb][e] *= alpha;
+#pragma unroll
+          for (int e = 0; e < 16; ++e) sc[qb][e] -= d;
         }
-        const float nm = -m_run[qb];
         float psum = 0.0f;
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
-          const float p = __builtin_amdgcn_exp2f(fmaf(sc[qb][e], c, nm));
-          if constexpr (!C::MFMA_SUM) psum += p;
+          const float p = __builtin_amdgcn_exp2f(sc[qb][e]);
+          if constexpr (!C::MFMA_SUM) psum = e ? psum + p : p;   // no add of 0 to start
           pb[qb][e >> 3][e & 7] = (bf16)p;
         }
         if constexpr (!C::MFMA_SUM) l_part[qb] += psum;
@@ -300,12 +313,12 @@ __global__ __launch_bounds__(QTILE / QB * 2) void attn_bf16_dma_kernel(AttnArgs 
       if (nkb == 2) scores(1, sb);
       read_v(0, va);
       __builtin_amdgcn_sched_barrier(0);
-      softmax(0, sa, pa);
+      softmax(0, t == 0, sa, pa);
       pv(va, pa);
       if (nkb == 2) {
         __builtin_amdgcn_sched_barrier(0);
         read_v(1, va);
-        softmax(1, sb, pa);
+        softmax(1, false, sb, pa);
         pv(va, pa);
       }
     } else {
@@ -316,11 +329,11 @@ __global__ __launch_bounds__(QTILE / QB * 2) void attn_bf16_dma_kernel(AttnArgs 
         f32x16 sc[QB];
         scores(kb, sc);
         if constexpr (C::V_DIRECT) {
-          softmax(kb, sc, pa);
+          softmax(kb, t == 0 && kb == 0, sc, pa);
           pv_direct(kb, pa);
         } else {
           read_v(kb, va);
-          softmax(kb, sc, pa);
+          softmax(kb, t == 0 && kb == 0, sc, pa);
           pv(va, pa);
         }
       }
