@@ -83,6 +83,7 @@ TRAFFIC_SOURCES = {
     "gemm_bf16_256x256": ("gemm_bf16.hip", "common.h", "eas_api.cpp"),
     "gemm_bf16_128x128": ("gemm_bf16.hip", "common.h", "eas_api.cpp"),
     "gemm_bf16_async_256x256": ("gemm_bf16.hip", "common.h", "eas_api.cpp"),
+    "gemm_bf16_async_res_256x256": ("gemm_bf16.hip", "common.h", "eas_api.cpp"),
     "gemm_bf16_async_128x128": ("gemm_bf16.hip", "common.h", "eas_api.cpp"),
     "gemm_bf16_64x64": ("gemm_bf16.hip", "common.h", "eas_api.cpp"),
     "gemm_bf16_64x128": ("gemm_bf16.hip", "common.h", "eas_api.cpp"),

@@ -31,9 +31,9 @@
 //    accumulators, then every lane owns 8 consecutive columns of a row and
 //    applies bias, GELU / QuickGELU, a position-table row and the fp32
 //    residual before one 16-byte (bf16) or 2 x 16-byte (fp32) store.
-//  * Bias / activation epilogues with up to 2048-wide k run a persistent
-//    variant (below) whose epilogue stores keep draining while the next
-//    tile's k-loop runs.
+//  * Bias / activation epilogues with up to 2048-wide k, and fp32 residual
+//    epilogues (O-projection, FC2) of any k, run a persistent variant (below)
+//    whose epilogue stores keep draining while the next tile's k-loop runs.
 //  * Every output element accumulates k in the same order (16-wide MFMA
 //    slices, ascending) whatever the kernel, tile shape or M, so a
 //    request's result does not depend on what else is in the micro-batch.
@@ -43,6 +43,7 @@ namespace eas {
 namespace {
 
 constexpr int BK = 64;
+constexpr int kResAhead = 1;   // residual epilogue: blocks of residual loads in flight ahead of the one in use
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
 // M0 carries the LDS base of each DMA; nothing else in these kernels uses M0
@@ -319,7 +320,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_tile_kernel(GemmArgs
   }
 }
 
-// ---- persistent variant with an asynchronous epilogue (bias and activation only) ----
+// ---- persistent variant with an asynchronous epilogue (bias, activation, fp32 residual) ----
 //
 // A fixed grid of workgroups walks the tile list (block b takes tiles b, b + grid,
 // ...; the same XCD-aware order as above), so a CU moves to its next tile
@@ -347,11 +348,13 @@ struct ACfg : Cfg<BM, BN, WGM, WGN> {
   __device__ static int sw16(int row) { return (row >> 2) & 3; }   // 16-byte chunk swizzle of 64-byte rows
 };
 
-template <int BM, int BN, int WGM, int WGN, int OUTF32>
+template <int BM, int BN, int WGM, int WGN, int OUTF32, int RES = 0>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_async_kernel(GemmArgs a, int n_tiles) {
   using C = ACfg<BM, BN, WGM, WGN, OUTF32>;
   constexpr int S = C::FM * C::FN * 2 * (OUTF32 ? 2 : 1);   // buffer stores per wave per tile
+  constexpr int L = RES ? C::FM * C::FN * 4 : 0;              // residual loads per wave per tile
   static_assert(C::DPS + S + 1 < 64, "vmcnt range");
+  static_assert(!RES || OUTF32, "the residual stream is fp32");
   extern __shared__ __attribute__((aligned(1024))) char smem[];
   const unsigned lds0 = (unsigned)(size_t)((__attribute__((address_space(3))) char*)smem);
   const int tid = threadIdx.x, lane = tid & 63;
@@ -448,8 +451,11 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_async_kernel(GemmArg
     const bool has_next = tn < n_tiles;
     int m0n = 0, n0n = 0;
     if (has_next) tile_of(tn, m0n, n0n);
-    // k-tile 0: issued ahead of k-tile 1 and of the previous tile's S stores
+    // k-tile 0: issued ahead of k-tile 1 and of the previous tile's S stores (with a
+    // residual: ahead of the previous epilogue's L loads and S stores, then k-tile 1;
+    // a count past vmcnt's range waits for a few loads that have completed anyway)
     if (first) wait_vm<C::DPS>();
+    else if constexpr (RES) wait_vm<(C::DPS + L + S < 63 ? C::DPS + L + S : 63)>();
     else wait_vm<C::DPS + S>();
     __builtin_amdgcn_s_barrier();
     issue_bias(n0);
@@ -470,8 +476,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_async_kernel(GemmArg
       }
       wait_lds();
       // k-tile kt+1 has landed; at kt == 0 the previous stores and the bias DMA may follow it
+      // (with a residual, k-tile 1 follows the previous epilogue: only the bias DMA)
       if (kt == 0) {
-        if (first) wait_vm<1>();
+        if (first || RES) wait_vm<1>();
         else wait_vm<S + 1>();
       } else {
         wait_vm<0>();
@@ -488,8 +495,35 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_async_kernel(GemmArg
       mma(fa[(NH - 1) & 1], fb[(NH - 1) & 1]);
       interleave();
     }
+    // Residual epilogue: each lane adds 8 fp32 residual values per 16-row pass, two
+    // passes per 32 x 32 block; a block's 4 loads are issued up to kResAhead blocks
+    // ahead (the first block's under the last k-step).  The loads are ordinary buffer
+    // loads, so the compiler waits for them itself: no DMA is issued between them
+    // and their use, so its counts are exact.  Rows past M and columns past N read 0.
+    const int prow = lane >> 2, pc = (lane & 3) * 8;
+    const int rows = min(BM, a.M - m0);
+    constexpr int NB = C::FM * C::FN, RR = kResAhead + 1;
+    u32x4 rq[RR][2][2];   // [block % RR][pass][half]
+    __amdgpu_buffer_rsrc_t res_rsrc;
+    if constexpr (RES)
+      res_rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(a.resid) + (size_t)m0 * a.ldr, 0,
+                                                   rows * a.ldr * 4, 0x00020000);
+    auto rload = [&](int b, u32x4 (&r)[2][2]) {
+      const int i = b / C::FN, j = b % C::FN;
+      const int n = n0 + wn * C::WN + j * 32 + pc;
+#pragma unroll
+      for (int p = 0; p < 2; ++p) {
+        const int mr = wm * C::WM + i * 32 + p * 16 + prow;
+        // bit 31 set for columns past N (the sign of N - 1 - n), without a select,
+        // which the compiler would turn into a branch around each pair of loads
+        const unsigned off = (unsigned)((mr * a.ldr + n) * 4) | ((unsigned)(a.N - 1 - n) & 0x80000000u);
+        r[p][0] = __builtin_amdgcn_raw_buffer_load_b128(res_rsrc, off, 0, 0);
+        r[p][1] = __builtin_amdgcn_raw_buffer_load_b128(res_rsrc, off + 16, 0, 0);
+      }
+    };
     {
       const int st = (sb + KT - 1) & 1;
+      if constexpr (RES) rload(0, rq[0]);
 #pragma unroll
       for (int h = 0; h < NH - 1; ++h) {
         load_frags(st, cofs[h + 1], fa[(h + 1) & 1], fb[(h + 1) & 1]);
@@ -500,20 +534,18 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_async_kernel(GemmArg
     }
     wait_lds();
     // the bias has landed: with KT > 2 the wait of k-step 1 covered it; with KT == 2
-    // only the next tile's k-tile 0 was issued after it
+    // only the next tile's k-tile 0 (and the first residual loads) were issued after it
     if (KT == 2) {
-      if (has_next) wait_vm<C::DPS>();
-      else wait_vm<0>();
+      if (has_next) wait_vm<C::DPS + L / (C::FM * C::FN)>();
+      else wait_vm<L / (C::FM * C::FN)>();
     }
     __builtin_amdgcn_s_barrier();   // every wave is past the last stage
-    if (has_next) issue(1, (sb + KT + 1) & 1);
+    if (!RES && has_next) issue(1, (sb + KT + 1) & 1);
     __builtin_amdgcn_sched_barrier(0);
 
     // ---- epilogue: one 32 x 32 block at a time through the wave's slab ----
-    const int rows = min(BM, a.M - m0);
     const __amdgpu_buffer_rsrc_t out_rsrc = __builtin_amdgcn_make_buffer_rsrc(
         static_cast<char*>(a.out) + (size_t)m0 * a.ldo * es, 0, rows * a.ldo * es, 0x00020000);
-    const int prow = lane >> 2, pc = (lane & 3) * 8;
     if constexpr (!OUTF32) {
       // bf16 output: bias and activation on the sums in place (columns 8q + 4g + e
       // of each block), then the finished 32 x 32 bf16 block goes through the slab
@@ -566,6 +598,15 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_async_kernel(GemmArg
     for (int i = 0; i < C::FM; ++i) {
 #pragma unroll
       for (int j = 0; j < C::FN; ++j) {
+        const int b = i * C::FN + j;
+        if constexpr (RES) {
+          // loads reach min(b + 1, kResAhead) blocks ahead of block b: the
+          // look-ahead grows as finished blocks free their accumulators
+          const int upto_prev = b == 0 ? 0 : min(NB - 1, b - 1 + min(b, kResAhead));
+          const int upto = min(NB - 1, b + min(b + 1, kResAhead));
+#pragma unroll
+          for (int d = upto_prev + 1; d <= upto; ++d) rload(d, rq[d % RR]);
+        }
         // acc element 4q + e sits at row lrow, column 8q + 4g + e of the block
 #pragma unroll
         for (int q = 0; q < 4; ++q)
@@ -596,6 +637,10 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_async_kernel(GemmArg
 #pragma unroll
             for (int e = 0; e < 8; ++e) v[e] = quick_gelu(v[e]);
           }
+          if constexpr (RES) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) v[e] += __uint_as_float(rq[b % RR][p][e >> 2][e & 3]);
+          }
           // rows past M fall outside the buffer's range; columns past N are sent out of range
           const unsigned off = n < a.N ? (unsigned)((mr * a.ldo + n) * es) : 0x80000000u;
           if (OUTF32) {
@@ -614,6 +659,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_async_kernel(GemmArg
         }
       }
     }
+    }
+    if constexpr (RES) {
+      if (has_next) issue(1, (sb + KT + 1) & 1);   // after the epilogue's loads (see above)
     }
     if (!has_next) break;
     wait_lds();   // the slab reads are done before the next bias DMA rewrites it
@@ -640,10 +688,10 @@ hipError_t launch_tile(const GemmArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <int BM, int BN, int WGM, int WGN, int OUTF32>
+template <int BM, int BN, int WGM, int WGN, int OUTF32, int RES = 0>
 hipError_t launch_async_t(const GemmArgs& a, hipStream_t s) {
   using C = ACfg<BM, BN, WGM, WGN, OUTF32>;
-  auto kern = gemm_bf16_async_kernel<BM, BN, WGM, WGN, OUTF32>;
+  auto kern = gemm_bf16_async_kernel<BM, BN, WGM, WGN, OUTF32, RES>;
   static int slots = 0;   // co-resident workgroups on this device, found once per instantiation
   if (!slots) {
     hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
@@ -686,6 +734,11 @@ bool tile_ok(const GemmArgs& a) {
 // to 32 k-tiles.  Past that the epilogue is a small share of a tile and the
 // per-tile kernel measured slightly faster (both give the same bits).
 bool async_ok(const GemmArgs& a) { return tile_ok(a) && !a.resid && !a.pos && a.K >= 2 * BK && a.K <= 32 * BK; }
+
+// Its residual form (fp32 residual stream, fp32 output: O-projection and FC2), any
+// K: the residual read and write are a large share of such a tile, and the
+// stores drain under the next tile's k-loop.
+bool async_res_ok(const GemmArgs& a) { return tile_ok(a) && a.resid && a.out_f32 && !a.pos && a.K >= 2 * BK; }
 
 }  // namespace
 
@@ -748,6 +801,10 @@ hipError_t launch_gemm_bf16(const GemmArgs& a, hipStream_t s, const char** kname
     }
     *kname = "gemm_bf16_64x128";
     return launch_tile<64, 128, 2, 2, 3>(a, s);
+  }
+  if (async_res_ok(a) && best_tile(a.M, a.N, nullptr) == 0) {
+    *kname = "gemm_bf16_async_res_256x256";   // 8 waves of 64 x 128: 4 KB fp32 slabs
+    return launch_async_t<256, 256, 4, 2, 1, 1>(a, s);
   }
   if (async_ok(a)) switch (best_tile(a.M, a.N, nullptr)) {
       case 0:   // 16 waves of 64 x 64 with bf16 output (2 KB slabs); the fp32 slabs need 8 waves
