@@ -137,6 +137,26 @@ def test_full_depth_clip_microbatch_sampled_request():
     assert e <= TOL["bf16"], e
 
 
+def test_widths_that_end_in_a_partial_column_tile():
+    """A CLIP-style encoder 832 wide (13 heads of 64, MLP 3328), one layer, 28
+    images (16156 tokens, one micro-batch run whole): the QKV GEMM (2496
+    columns) and the O-projection and FC2 (832 columns) end in a partly
+    filled 256-column tile, so the persistent GEMMs drop columns past N (the
+    presets' widths are all multiples of 256).  Requests 0, 13 and 27 against
+    the reference run on each image alone."""
+    p = dict(C.with_layers(C.CLIP_L336, 1), name="clip_style_w832_L1", hidden=832, heads=13, mlp=3328,
+             out_dim=832)
+    W = synth.make_weights(p, 0)
+    items = synth.make_items(p, 28, 0)
+    got = gpu_encode(p, items, W)
+    cu = got["cu_out"]
+    assert int(got["cu"][-1]) == 28 * 577
+    for r in (0, 13, 27):
+        e = rel_err(got["out"][cu[r]:cu[r + 1]], oracle_encode(p, [items[r]], W)["out"])
+        print("[parity] width 832, request %d: relative error %.3g" % (r, e), flush=True)
+        assert e <= TOL["bf16"], (r, e)
+
+
 def test_bf16_output_dtype():
     p = C.with_layers(C.CLIP_L336, 1)
     W = synth.make_weights(p, 0)
