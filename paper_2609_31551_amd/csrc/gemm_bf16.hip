@@ -730,15 +730,26 @@ bool tile_ok(const GemmArgs& a) {
   return true;
 }
 
+// The persistent kernel's buffer resources span one 256-row tile of the output
+// (and of the residual) with 32-bit sizes and offsets.
+bool tile_rows_fit(const GemmArgs& a) {
+  const double lim = 2147483648.0;
+  return 256.0 * a.ldo * (a.out_f32 ? 4 : 2) < lim && (!a.resid || 256.0 * a.ldr * 4 < lim);
+}
+
 // The persistent asynchronous-epilogue kernel: bias / activation epilogues, two
 // to 32 k-tiles.  Past that the epilogue is a small share of a tile and the
 // per-tile kernel measured slightly faster (both give the same bits).
-bool async_ok(const GemmArgs& a) { return tile_ok(a) && !a.resid && !a.pos && a.K >= 2 * BK && a.K <= 32 * BK; }
+bool async_ok(const GemmArgs& a) {
+  return tile_ok(a) && tile_rows_fit(a) && !a.resid && !a.pos && a.K >= 2 * BK && a.K <= 32 * BK;
+}
 
 // Its residual form (fp32 residual stream, fp32 output: O-projection and FC2), any
 // K: the residual read and write are a large share of such a tile, and the
 // stores drain under the next tile's k-loop.
-bool async_res_ok(const GemmArgs& a) { return tile_ok(a) && a.resid && a.out_f32 && !a.pos && a.K >= 2 * BK; }
+bool async_res_ok(const GemmArgs& a) {
+  return tile_ok(a) && tile_rows_fit(a) && a.resid && a.out_f32 && !a.pos && a.K >= 2 * BK;
+}
 
 }  // namespace
 
