@@ -18,9 +18,9 @@ bracketed by HIP events on the encoder's stream; the kernel with the largest
 total time is the dominant kernel, and its algorithmic flops per launch over
 its mean duration is compared with the bf16 dense MFMA peak.  The CPU
 baseline times the fp64 reference on a bounded sample (whole images, full
-depth) on the host cores; per-workload reference timings at micro-batch 1
-run at reduced depth where the full depth would exceed the time budget, and
-say so.
+depth) on the host cores, and on one request with one thread;
+per-workload reference timings at micro-batch 1 run at reduced depth where
+the full depth would exceed the time budget, and say so.
 """
 import argparse
 import hashlib
@@ -290,6 +290,22 @@ def cpu_config_timing(preset, wl, budget_s):
     return rec
 
 
+def cpu_one_thread(preset, wl):
+    """The reference on the pool's first request, full depth, with its BLAS
+    held to one thread (timed directly: each call converts every layer's
+    weights to float64, a fixed cost that drowns depth differences)."""
+    from threadpoolctl import threadpool_limits
+    from oracle import encoder as O
+    packed, cu, grid = O.pack(preset, [wl.items_host[0]])
+    tokens = int(cu[-1])
+    with threadpool_limits(limits=1):
+        t0 = time.time()
+        O.encode(preset, wl.weights_host, packed, cu, grid)
+        dt = time.time() - t0
+    return {"micro_batch": 1, "tokens": tokens, "cores": 1, "depth": preset["layers"], "seconds": dt,
+            "tokens_per_s": tokens / dt, "measured_full_depth": True}
+
+
 def service_times(rows, pool, bound):
     """Seconds per micro-batch of b requests, b = 1 .. bound, from the swept
     pass times (linear between measured sizes)."""
@@ -523,6 +539,7 @@ def main():
     cpu_configs = {}
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(preset, wl, args.batch, args.cpu_budget_s)
+        result["cpu_baseline"]["one_thread"] = cpu_one_thread(preset, wl)
         if args.cpu_configs_budget_s > 0:
             cpu_configs[preset["name"]] = cpu_config_timing(preset, wl, args.cpu_configs_budget_s)
     wl.close()
