@@ -137,6 +137,20 @@ def test_full_depth_clip_microbatch_sampled_request():
     assert e <= TOL["bf16"], e
 
 
+def test_qwen_images_of_extreme_aspect_ratio():
+    """Qwen-style images far outside the pool's aspect range (0.5..2): 56 x 1344
+    and 1344 x 56 (4 x 96 and 96 x 4 patch grids, 384 tokens each: RoPE at
+    row / column positions up to 95) and the smallest mergeable image, 28 x
+    28 (2 x 2 patches, one output row), in one micro-batch, two layers."""
+    p = C.with_layers(C.QWEN_IMAGE, 2)
+    W = synth.make_weights(p, 0)
+    items = _items(p, [(2, 56, 1344), (2, 1344, 56), (2, 28, 28)])
+    got = gpu_encode(p, items, W)
+    assert got["cu"].tolist() == [0, 384, 768, 772]
+    assert got["cu_out"].tolist() == [0, 96, 192, 193]
+    check_parity(p, got, oracle_encode(p, items, W))
+
+
 def test_widths_that_end_in_a_partial_column_tile():
     """A CLIP-style encoder 832 wide (13 heads of 64, MLP 3328), one layer, 28
     images (16156 tokens, one micro-batch run whole): the QKV GEMM (2496
