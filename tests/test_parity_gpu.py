@@ -151,6 +151,19 @@ def test_qwen_images_of_extreme_aspect_ratio():
     check_parity(p, got, oracle_encode(p, items, W))
 
 
+def test_video_clips_at_both_temporal_extremes():
+    """Video clips of 32 frames on a 56 x 56 grid (16 temporal positions of 4 x
+    4 patches: the 3D RoPE's time axis up to 15) and of 2 frames (a single
+    temporal patch, 8 x 8), in one micro-batch, two layers."""
+    p = C.with_layers(C.QWEN_VIDEO, 2)
+    W = synth.make_weights(p, 0)
+    items = _items(p, [(32, 56, 56), (2, 112, 112)])
+    got = gpu_encode(p, items, W)
+    assert got["cu"].tolist() == [0, 256, 320]
+    assert got["grid"].tolist() == [[16, 4, 4], [1, 8, 8]]
+    check_parity(p, got, oracle_encode(p, items, W))
+
+
 def test_widths_that_end_in_a_partial_column_tile():
     """A CLIP-style encoder 832 wide (13 heads of 64, MLP 3328), one layer, 28
     images (16156 tokens, one micro-batch run whole): the QKV GEMM (2496
