@@ -184,9 +184,13 @@ def test_widths_that_end_in_a_partial_column_tile():
         assert e <= TOL["bf16"], (r, e)
 
 
-def test_bf16_output_dtype():
-    p = C.with_layers(C.CLIP_L336, 1)
+@pytest.mark.parametrize("name", ["clip_vit_l14_336", "qwen2vl_vit_image", "whisper_large_enc"])
+def test_bf16_output_dtype(name):
+    """bf16 embeddings out of each final stage: the last layer's residual GEMM
+    (CLIP), the merger's second GEMM (Qwen-style), the final LayerNorm
+    (Whisper-style)."""
+    p = C.with_layers(C.PRESETS[name], 1)
     W = synth.make_weights(p, 0)
-    items = synth.make_items(p, 2, 0)
+    items = _items(p, SHAPES[name], 2)
     got = gpu_encode(p, items, W, out_dtype="bf16")
     check_parity(p, got, oracle_encode(p, items, W))
