@@ -95,7 +95,7 @@ def _peaked_weights(p, seed):
     return W
 
 
-@pytest.mark.parametrize("name", ["clip_vit_l14_336", "qwen2vl_vit_image"])
+@pytest.mark.parametrize("name", ["clip_vit_l14_336", "qwen2vl_vit_image", "qwen2vl_vit_video", "whisper_large_enc"])
 def test_peaked_attention_parity(name):
     p = C.with_layers(C.PRESETS[name], 1)
     W = _peaked_weights(p, 3)
