@@ -33,20 +33,25 @@ struct AttnWork {
 
 enum Act { ACT_NONE = 0, ACT_GELU = 1, ACT_QUICKGELU = 2 };
 
-// erf by Abramowitz & Stegun, Handbook of Mathematical Functions, formula
-// 7.1.26: erf(x) = 1 - (a1 t + a2 t^2 + a3 t^3 + a4 t^4 + a5 t^5) exp(-x^2),
-// t = 1 / (1 + p x) for x >= 0, |error| <= 1.5e-7, extended as an odd
-// function.  Branch-free: one reciprocal and one exponential instead of the
-// math library's two-range polynomial, in the GEMM epilogues where it runs
-// on every output element.
-__device__ __forceinline__ float erf_as7126(float x) {
-  const float ax = fabsf(x);
-  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, ax, 1.0f));
-  const float y =
-      t * fmaf(fmaf(fmaf(fmaf(1.061405429f, t, -1.453152027f), t, 1.421413741f), t, -0.284496736f), t, 0.254829592f);
-  return copysignf(fmaf(-y, __expf(-ax * ax), 1.0f), x);
+// GELU(v) = v Phi(v) = 0.5 v (1 + erf(v / sqrt 2)) with erf by Abramowitz &
+// Stegun, Handbook of Mathematical Functions, formula 7.1.28:
+// erf(x) = 1 - 1 / (1 + a1 x + ... + a6 x^6)^16 for x >= 0, |error| <= 3e-7.
+// With P(|v|) = that polynomial at |v| / sqrt 2 (the scale folded into the
+// coefficients), GELU(v) = max(v, 0) - 0.5 |v| / P^16 for either sign of v:
+// branch-free, one reciprocal and no exponential, in the GEMM epilogues where
+// it runs on every output element.  P^16 overflowing to inf for |v| > ~25
+// gives the exact limits (v, or -0).
+__device__ __forceinline__ float gelu_erf(float v) {
+  const float av = fabsf(v);
+  float p = fmaf(fmaf(fmaf(fmaf(fmaf(5.38297490e-06f, av, 4.88906371e-05f), av, 3.80035744e-05f), av,
+                           3.27762635e-03f), av, 2.11410057e-02f), av, 4.98673469e-02f);
+  p = fmaf(p, av, 1.0f);
+  p *= p;
+  p *= p;
+  p *= p;
+  p *= p;
+  return fmaxf(v, 0.0f) - 0.5f * av * __builtin_amdgcn_rcpf(p);
 }
-__device__ __forceinline__ float gelu_erf(float v) { return 0.5f * v * (1.0f + erf_as7126(v * 0.70710678118654752f)); }
 // x sigmoid(1.702 x), with the hardware reciprocal instead of a full-precision divide
 __device__ __forceinline__ float quick_gelu(float v) { return v * __builtin_amdgcn_rcpf(1.0f + __expf(-1.702f * v)); }
 __device__ __forceinline__ float apply_act(int act, float v) {
