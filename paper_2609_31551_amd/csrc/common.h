@@ -52,8 +52,11 @@ __device__ __forceinline__ float gelu_erf(float v) {
   p *= p;
   return fmaxf(v, 0.0f) - 0.5f * av * __builtin_amdgcn_rcpf(p);
 }
-// x sigmoid(1.702 x), with the hardware reciprocal instead of a full-precision divide
-__device__ __forceinline__ float quick_gelu(float v) { return v * __builtin_amdgcn_rcpf(1.0f + __expf(-1.702f * v)); }
+// x sigmoid(1.702 x) = x / (1 + 2^(-1.702 log2(e) x)): one multiply into the
+// hardware exponential, and the hardware reciprocal instead of a full-precision divide
+__device__ __forceinline__ float quick_gelu(float v) {
+  return v * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(v * -2.45546696f));
+}
 __device__ __forceinline__ float apply_act(int act, float v) {
   if (act == ACT_GELU) return gelu_erf(v);
   if (act == ACT_QUICKGELU) return quick_gelu(v);
