@@ -469,7 +469,7 @@ def main():
         # order, so encode work could sit behind the reservation (set before HIP starts)
         os.environ["GPU_MAX_HW_QUEUES"] = "16"
     if args.gpus != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path (requests shard by "
+        print("bench.py measures one GPU only: the library has no multi-GPU path (requests shard by "
               "micro-batch across independent encoders); run with --gpus 1", file=sys.stderr)
         sys.exit(2)
     if args.copy_calib_mib:
