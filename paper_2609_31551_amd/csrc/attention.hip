@@ -235,11 +235,14 @@ int attention_q_tile(int dtype_bf16) { return dtype_bf16 ? QT : QT32; }
 
 hipError_t launch_attention_bf16(const AttnArgs& a, const AttnWork& w, int total_tiles, int N, hipStream_t s,
                                  const char** kname) {
-  if (attention_dma_supported(a, N)) return launch_attention_bf16_dma(a, w, total_tiles, s, kname);
+  // head_dim 64 and 80 always take the DMA kernel: the library caps a handle's
+  // tokens so that its 32-bit offsets hold, and keeps the qkv rows 16-byte
+  // aligned, so one kernel (one summation order) serves every micro-batch
+  if (a.hd == 64 || a.hd == 80)
+    return attention_dma_supported(a, N) ? launch_attention_bf16_dma(a, w, total_tiles, s, kname)
+                                         : hipErrorInvalidValue;
   const dim3 grid((unsigned)(total_tiles * a.heads)), blk(256);
   switch (a.hd) {
-    case 64: *kname = "attn_bf16_staged_hd64"; hipLaunchKernelGGL((attn_bf16_kernel<64>), grid, blk, 0, s, a, w); break;
-    case 80: *kname = "attn_bf16_staged_hd80"; hipLaunchKernelGGL((attn_bf16_kernel<80>), grid, blk, 0, s, a, w); break;
     case 128: *kname = "attn_bf16_hd128"; hipLaunchKernelGGL((attn_bf16_kernel<128>), grid, blk, 0, s, a, w); break;
     case 16: *kname = "attn_bf16_hd16"; hipLaunchKernelGGL((attn_bf16_kernel<16>), grid, blk, 0, s, a, w); break;
     case 32: *kname = "attn_bf16_hd32"; hipLaunchKernelGGL((attn_bf16_kernel<32>), grid, blk, 0, s, a, w); break;

@@ -113,6 +113,17 @@ Layout build_layout(const eas_config& c) {
   return L;
 }
 
+// Elements per token of the widest activation buffer an encode pass uses as a
+// GEMM or attention operand: qkv (3d), the MLP hidden (mlp), the merger input
+// (4d), zero-padded patch rows, and the Whisper front end's im2col rows (two
+// conv1 input frames of 3 n_mels per token, 3d per conv2 output frame).
+int64_t widest_row(const eas_config& c) {
+  const int64_t d = c.hidden, kp = k_patch(c);
+  int64_t w = std::max<int64_t>({3 * d, (int64_t)c.mlp, 4 * d, (kp + 63) / 64 * 64});
+  if (c.kind == EAS_KIND_WHISPER) w = std::max<int64_t>(w, 6 * (int64_t)c.n_mels);
+  return w;
+}
+
 // Returns "" when the config is usable, else the reason.
 std::string check_config(const eas_config& c, eas_status* st) {
   *st = EAS_ERR_INVALID_ARG;
@@ -154,6 +165,10 @@ std::string check_config(const eas_config& c, eas_status* st) {
     return "bf16 head_dim must be 16, 32, 64, 80 or 128";
   if (c.dtype == EAS_FP32 && c.head_dim != 16 && c.head_dim != 32 && c.head_dim != 64 && c.head_dim != 80)
     return "fp32 head_dim must be 16, 32, 64 or 80";
+  // The bf16 GEMM and attention kernels address each operand with 32-bit byte
+  // offsets; every per-token buffer stays below 2^31 elements (4 GiB of bf16).
+  if ((double)c.max_tokens * (double)widest_row(c) >= 2147483648.0)
+    return "max_tokens too large: the widest per-token buffer would reach 2^31 elements";
   *st = EAS_OK;
   return "";
 }
@@ -252,6 +267,7 @@ struct eas_encoder {
   int64_t ao_w = 0, hw = 0;  // elements per token of ao and hbuf
   hipStream_t side = nullptr;                          // second half of a split micro-batch
   hipEvent_t ev_fork = nullptr, ev_join = nullptr;
+  hipEvent_t ev_done = nullptr;   // recorded on the caller's stream after each encode call
 
   Workspace rows_from(int64_t r0) const {
     const int64_t d = cfg.hidden, el = cfg.dtype == EAS_BF16 ? 2 : 4;
@@ -771,7 +787,13 @@ eas_status eas_encoder_create(const eas_config* cfg, eas_encoder** out) {
       e->ev_fork = nullptr;
     }
   }
+  if (herr == hipSuccess) herr = hipEventCreateWithFlags(&e->ev_done, hipEventDisableTiming);
   if (herr != hipSuccess) {
+    if (e->side) {
+      (void)hipEventDestroy(e->ev_fork);
+      (void)hipEventDestroy(e->ev_join);
+      (void)hipStreamDestroy(e->side);
+    }
     (void)hipFree(e->ws);
     delete e;
     return EAS_ERR_HIP;
@@ -782,12 +804,18 @@ eas_status eas_encoder_create(const eas_config* cfg, eas_encoder** out) {
 
 void eas_encoder_destroy(eas_encoder* enc) {
   if (!enc) return;
-  (void)hipDeviceSynchronize();
+  // only the handle's own work: the last encode call ends with ev_done on the
+  // caller's stream (its second half, if any, joined that stream before it;
+  // earlier calls were ordered before it, as calls on one handle must be), and
+  // the side stream is the handle's own
+  if (enc->ev_done) (void)hipEventSynchronize(enc->ev_done);
+  if (enc->side) (void)hipStreamSynchronize(enc->side);
   for (auto& r : enc->recs) {
     (void)hipEventDestroy(r.e0);
     (void)hipEventDestroy(r.e1);
   }
   for (auto ev : enc->pool) (void)hipEventDestroy(ev);
+  if (enc->ev_done) (void)hipEventDestroy(enc->ev_done);
   if (enc->side) {
     (void)hipEventDestroy(enc->ev_fork);
     (void)hipEventDestroy(enc->ev_join);
@@ -917,6 +945,7 @@ eas_status eas_encode_microbatch(eas_encoder* enc, const void* packed_in, const 
                         hipStreamWaitEvent(s, enc->ev_join, 0) == hipSuccess;
     if (rc == EAS_OK && !joined) rc = fail(enc, EAS_ERR_HIP, "stream join failed");
   }
+  if (hipEventRecord(enc->ev_done, s) != hipSuccess && rc == EAS_OK) rc = fail(enc, EAS_ERR_HIP, "event record failed");
   if (rc != EAS_OK) return rc;
   if (cu_out) {
     for (int r = 0; r <= n_seqs; ++r) cu_out[r] = c.merge == 2 ? cu_seqlens[r] / 4 : cu_seqlens[r];

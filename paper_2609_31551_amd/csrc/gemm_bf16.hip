@@ -849,9 +849,7 @@ int gemm_bf16_head_rows(const GemmArgs& a) {
 GemmArgs gemm_rows(const GemmArgs& a, int m0, int m1) {
   GemmArgs r = a;
   r.M = m1 - m0;
-  const size_t ea = a.stats ? 4 : 2;   // fp32 rows when the LayerNorm is applied on the fly
-  r.A = static_cast<const char*>(a.A) + (size_t)m0 * a.lda * ea;
-  if (a.stats) r.stats = a.stats + (size_t)m0 * a.ln_group;
+  r.A = static_cast<const char*>(a.A) + (size_t)m0 * a.lda * 2;
   r.out = static_cast<char*>(a.out) + (size_t)m0 * a.ldo * (a.out_f32 ? 4 : 2);
   if (a.resid) r.resid = a.resid + (size_t)m0 * a.ldr;
   if (a.pos_idx) r.pos_idx = a.pos_idx + m0;

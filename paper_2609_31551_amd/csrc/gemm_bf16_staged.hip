@@ -1,7 +1,7 @@
 // Register-staged bf16 MFMA GEMM: the path for operands the DMA-fed tile
 // kernel (gemm_bf16.hip) cannot take -- rows that are not 16-byte aligned or
-// K not a multiple of its k-step (the patch embedding, K = 588 / 1176) -- and
-// the LayerNorm-prologue form.  Same contract: C[m, n] = sum_k A[m, k] * B[n, k].
+// K not a multiple of its k-step (widths that are multiples of 8 but not of
+// 64).  Same contract: C[m, n] = sum_k A[m, k] * B[n, k].
 //
 // Design (gfx950):
 //  * v_mfma_f32_32x32x16_bf16: each lane feeds 8 consecutive k of one row of
@@ -14,9 +14,6 @@
 //    of step k and written to the other stage after them, so one barrier per
 //    k-step suffices.  LDS rows are padded by 16 bytes so the 32 rows one
 //    16-byte read touches land on distinct banks.
-//  * LayerNorm prologue: with `stats`, A is the fp32 residual stream and the
-//    loader applies (x - mean) * rstd * g + b before rounding to bf16, so no
-//    normalised copy of the activations ever goes to HBM.
 //  * Fused epilogue: bias, GELU / QuickGELU, position-table add and fp32
 //    residual add, then one store (fp32 or bf16).  Accumulators go through
 //    LDS one 32-row slab per wave, so the residual reads and the output
@@ -53,7 +50,7 @@ __device__ __forceinline__ uint4 load8_checked(const bf16* base, int ld, int r, 
   return v.u;
 }
 
-template <int BM, int BN, int WM, int WN, bool LN, bool GENERIC>
+template <int BM, int BN, int WM, int WN, bool GENERIC>
 __global__ __launch_bounds__(64 * (BM / WM) * (BN / WN)) void gemm_bf16_kernel(GemmArgs a) {
   using T = Tile<BM, BN, WM, WN>;
   __shared__ __attribute__((aligned(16))) bf16 smem[2 * T::STAGE];
@@ -65,14 +62,10 @@ __global__ __launch_bounds__(64 * (BM / WM) * (BN / WN)) void gemm_bf16_kernel(G
   const int KT = (a.K + BK - 1) / BK;
 
   const bf16* Ab = static_cast<const bf16*>(a.A);
-  const float* Af = static_cast<const float*>(a.A);
   const bf16* Bb = static_cast<const bf16*>(a.B);
 
   // staging registers for one stage
-  uint4 ra[LN ? 1 : T::A_CH];
-  float4 rf[LN ? 2 * T::A_CH : 1];
-  float2 rst[LN ? T::A_CH : 1];
-  uint4 rg, rb;
+  uint4 ra[T::A_CH];
   uint4 rbw[T::B_CH];
 
   auto load_stage = [&](int kt) {
@@ -81,18 +74,7 @@ __global__ __launch_bounds__(64 * (BM / WM) * (BN / WN)) void gemm_bf16_kernel(G
     for (int i = 0; i < T::A_CH; ++i) {
       const int c = tid + i * T::NT, row = c / T::CPR, kc = (c % T::CPR) * 8;
       const int gm = m0 + row, gk = k0 + kc;
-      if constexpr (LN) {
-        const int r = gm < a.M ? gm : a.M - 1;
-        const float* p = Af + (long)r * a.lda + gk;
-        rf[2 * i] = *reinterpret_cast<const float4*>(p);
-        rf[2 * i + 1] = *reinterpret_cast<const float4*>(p + 4);
-        rst[i] = a.stats[(long)r * a.ln_group + gk / a.ln_dim];
-        if (i == 0) {
-          const int kk = gk % a.ln_dim;
-          rg = load16(static_cast<const bf16*>(a.ln_g) + kk);
-          rb = load16(static_cast<const bf16*>(a.ln_b) + kk);
-        }
-      } else if constexpr (GENERIC) {
+      if constexpr (GENERIC) {
         ra[i] = load8_checked(Ab, a.lda, gm, a.M, gk, a.K);
       } else {
         const int r = gm < a.M ? gm : a.M - 1;
@@ -118,18 +100,7 @@ __global__ __launch_bounds__(64 * (BM / WM) * (BN / WN)) void gemm_bf16_kernel(G
 #pragma unroll
     for (int i = 0; i < T::A_CH; ++i) {
       const int c = tid + i * T::NT, row = c / T::CPR, kc = (c % T::CPR) * 8;
-      if constexpr (LN) {
-        union { uint4 u; bf16 h[8]; } g, b, o;
-        g.u = rg; b.u = rb;
-        const float x[8] = {rf[2 * i].x, rf[2 * i].y, rf[2 * i].z, rf[2 * i].w,
-                            rf[2 * i + 1].x, rf[2 * i + 1].y, rf[2 * i + 1].z, rf[2 * i + 1].w};
-#pragma unroll
-        for (int e = 0; e < 8; ++e)
-          o.h[e] = (bf16)((x[e] - rst[i].x) * rst[i].y * (float)g.h[e] + (float)b.h[e]);
-        *reinterpret_cast<uint4*>(As + row * LDK + kc) = o.u;
-      } else {
-        *reinterpret_cast<uint4*>(As + row * LDK + kc) = ra[i];
-      }
+      *reinterpret_cast<uint4*>(As + row * LDK + kc) = ra[i];
     }
 #pragma unroll
     for (int i = 0; i < T::B_CH; ++i) {
@@ -212,10 +183,10 @@ __global__ __launch_bounds__(64 * (BM / WM) * (BN / WN)) void gemm_bf16_kernel(G
   }
 }
 
-template <int BM, int BN, int WM, int WN, bool LN, bool GENERIC>
+template <int BM, int BN, int WM, int WN, bool GENERIC>
 hipError_t launch_cfg(const GemmArgs& a, hipStream_t s) {
   const long tiles = (long)((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
-  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN, LN, GENERIC>), dim3((unsigned)tiles),
+  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN, GENERIC>), dim3((unsigned)tiles),
                      dim3(Tile<BM, BN, WM, WN>::NT), 0, s, a);
   return hipGetLastError();
 }
@@ -223,20 +194,17 @@ hipError_t launch_cfg(const GemmArgs& a, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_gemm_bf16_staged(const GemmArgs& a, hipStream_t s, const char** kname) {
-  const bool ln = a.stats != nullptr;
+  // bf16 models apply LayerNorm in a pass of its own (launch_ln_apply): the
+  // operands here are always bf16 rows
+  if (a.stats) return hipErrorInvalidValue;
   const bool aligned = (a.K % BK == 0) && (a.lda % 8 == 0) && (a.ldb % 8 == 0) &&
-                       ((uintptr_t)a.A % 16 == 0) && ((uintptr_t)a.B % 16 == 0) && (!ln || a.ln_dim % 8 == 0);
+                       ((uintptr_t)a.A % 16 == 0) && ((uintptr_t)a.B % 16 == 0);
   if (!aligned) {
-    if (ln) return hipErrorInvalidValue;   // the LN prologue needs the aligned path
     *kname = "gemm_bf16_generic_128x128";
-    return launch_cfg<128, 128, 64, 64, false, true>(a, s);
-  }
-  if (ln) {
-    *kname = "gemm_bf16_ln_128x128";
-    return launch_cfg<128, 128, 64, 64, true, false>(a, s);
+    return launch_cfg<128, 128, 64, 64, true>(a, s);
   }
   *kname = "gemm_bf16_staged_128x128";
-  return launch_cfg<128, 128, 64, 64, false, false>(a, s);
+  return launch_cfg<128, 128, 64, 64, false>(a, s);
 }
 
 }  // namespace eas

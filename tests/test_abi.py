@@ -98,7 +98,28 @@ def test_config_errors_are_reported_without_hip():
     with pytest.raises(eas.EasError):
         eas.weights_layout(eas.make_config(dict(C.QWEN_IMAGE, rope_sections=(0, 20, 19)), max_tokens=10))
     with pytest.raises(eas.EasError):
-        eas.microbatch_shape(eas.make_config(C.QWEN_IMAGE, max_tokens=10 ** 6), [[2, 3, 230, 308]])
+        eas.microbatch_shape(eas.make_config(C.QWEN_IMAGE, max_tokens=10 ** 5), [[2, 3, 230, 308]])
+
+
+@pytest.mark.parametrize("preset", [C.CLIP_L336, C.QWEN_IMAGE, C.WHISPER_L, C.TINY], ids=lambda p: p["name"])
+def test_max_tokens_is_capped_where_32_bit_offsets_end(preset):
+    """A handle's widest per-token buffer (MLP hidden, qkv, merger input,
+    padded patch rows) stays below 2^31 elements, so every bf16 kernel's
+    32-bit byte offsets hold and no micro-batch size changes the kernel (and
+    so the bits) a request gets.  Refused with UNSUPPORTED beyond that, on the
+    host, before any HIP call."""
+    d, f = preset["hidden"], preset["mlp"]
+    widest = max(3 * d, f, 4 * d, (C.k_patch(preset) + 63) // 64 * 64)
+    if preset["kind"] == C.KIND_WHISPER:
+        widest = max(widest, 6 * preset["n_mels"])
+    limit = (2 ** 31 - 1) // widest      # largest accepted max_tokens
+    ok = eas.make_config(preset, max_tokens=limit, max_seqs=2)
+    assert eas.weights_layout(ok)[1] > 0
+    for mt in (limit + 1, 2 ** 30):
+        cfg = eas.make_config(preset, max_tokens=mt, max_seqs=2)
+        assert eas.validate_microbatch(cfg, [0, 4], [[1, 2, 2]]) == eas.EAS_ERR_UNSUPPORTED
+    if preset is C.QWEN_IMAGE:
+        assert limit == 419430             # 32 of the largest images (9216 tokens) fit
 
 
 def test_every_router_symbol_is_exported():
