@@ -162,6 +162,30 @@ eas_status eas_encode_microbatch(eas_encoder* enc, const void* packed_in, const 
                                  const int32_t* grid_thw, int32_t n_seqs, const void* weights,
                                  void* out_embeddings, int32_t* cu_out, void* stream);
 
+/* For callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.  The same
+ * Encode pass as eas_encode_microbatch, with the same arguments except that
+ * *cfg takes the place of a handle: no eas_encoder_create, and the call makes
+ * no hipMalloc / hipFree and no other allocating call.  Its per-token
+ * workspace lives in a fixed device array of EAS_NOALLOC_SCRATCH_BYTES that
+ * the library holds on every device it runs on until the process ends.
+ * A micro-batch whose workspace does not fit is refused with
+ * EAS_ERR_CAPACITY before anything is enqueued (256 MiB holds about 11,800
+ * CLIP ViT-L tokens, 9,400 Qwen-style ViT tokens -- one 1344 x 1344 image --
+ * or six Whisper-large clips).  The micro-batch always runs as one pass on
+ * `stream` (no second stream), and profiling does not apply.  Every call on a
+ * device shares that device's array and leaves its contents behind; no
+ * buffer in it needs to start at zero (every kernel writes what it later
+ * reads).  Calls that overlap on one device -- on different streams, or from
+ * different threads -- race on the array: the caller orders them.  The
+ * output bits equal eas_encode_microbatch's for the same inputs.
+ * Errors as eas_encode_microbatch (no handle, so no eas_last_error detail);
+ * EAS_ERR_HIP if the array's device address cannot be looked up. */
+#define EAS_NOALLOC_SCRATCH_BYTES (256u << 20)
+eas_status eas_encode_microbatch_noalloc(const eas_config* cfg, const void* packed_in, const int32_t* cu_seqlens,
+                                         const int32_t* grid_thw, int32_t n_seqs, const void* weights,
+                                         void* out_embeddings, int32_t* cu_out, void* stream);
+
 /* Kernel timing for measurement.  While enabled, every launch the handle makes
  * is bracketed by HIP events on its stream.  eas_profile_read waits for the
  * recorded events and returns, per kernel, the number of launches, the summed

@@ -131,6 +131,10 @@ hipError_t launch_ln_apply(const float* x, int N, int d, float eps, const void* 
                            void* y, int y_f32, hipStream_t s);
 hipError_t launch_rope(void* qkv, int ldqkv, int N, int heads, int hd, int is_bf16, const int4* pos3,
                        const float* inv_freq, const int* slot_axis, hipStream_t s);
+// Whisper-style sinusoid position table [F, d] (fp32) and the rotary slot
+// tables (inverse frequency and axis of each of the sections' slots).
+hipError_t launch_sinusoid_table(float* tab, int F, int d, hipStream_t s);
+hipError_t launch_rope_table(float* inv_freq, int* slot_axis, const int sections[3], float theta, hipStream_t s);
 hipError_t launch_cls(const SeqMeta& m, float* x, int d, const void* cls, const void* pos0, int w_bf16,
                       hipStream_t s);
 // [rows, k] 16-bit rows copied to [rows, kp] (kp % 8 == 0, dst 16-byte aligned), zero-filled past k.

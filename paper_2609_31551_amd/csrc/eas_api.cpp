@@ -16,6 +16,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -24,6 +25,12 @@
 #include "common.h"
 
 using namespace eas;
+
+// Workspace of eas_encode_microbatch_noalloc: one array per device, part of
+// the library's device code object, so no call allocates.  Host code never
+// uses its name except to look up its device address (scratch_base); the
+// kernels get that address as an argument, like any workspace pointer.
+static __device__ __align__(256) char scratch[EAS_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
@@ -281,6 +288,72 @@ struct eas_encoder {
 };
 
 namespace {
+
+// Bytes of each workspace buffer of an encode pass over up to n tokens, in
+// the order bind_workspace lays them out (each 256-byte aligned).
+struct WsPlan {
+  int64_t sz[11];
+  int64_t total = 0;
+  int64_t ao_w = 0, hw = 0;   // elements per token of ao and hbuf
+  int kpad = 0;
+};
+
+WsPlan plan_workspace(const eas_config& c, int64_t n) {
+  WsPlan w;
+  const int64_t d = c.hidden, el = c.dtype == EAS_BF16 ? 2 : 4;
+  const int64_t hw = std::max<int64_t>({c.mlp, 4 * d, 3 * d});
+  int64_t qkv_rows = n, ao_rows = n;
+  if (c.kind == EAS_KIND_WHISPER) {   // front-end im2col and conv1 output reuse qkv / ao
+    qkv_rows = std::max<int64_t>(n, (2 * n * d + 3 * d - 1) / (3 * d));
+    ao_rows = std::max<int64_t>(n, (2 * n * 3 * c.n_mels + d - 1) / d);
+  }
+  auto al = [](int64_t b) { return (b + 255) / 256 * 256; };
+  const int64_t half = d / c.heads / 2;
+  // bf16 ViTs whose patch row is not a whole number of 64-element k-tiles run the
+  // embedding GEMM on zero-padded copies (rows in hbuf, weight in patch_w)
+  const int64_t kp = k_patch(c), kpad = (kp + 63) / 64 * 64;
+  if (c.dtype == EAS_BF16 && c.kind != EAS_KIND_WHISPER && kp % 64 && kpad <= hw) w.kpad = (int)kpad;
+  const int64_t sz[11] = {al(n * d * 4), al(n * 8), al(qkv_rows * 3 * d * el), al(ao_rows * d * el),
+                          al(n * hw * el), al(n * 16), al(n * 4),
+                          al(c.kind == EAS_KIND_WHISPER ? (int64_t)c.n_frames / 2 * d * 4 : 256),
+                          al(half * 8 + 256), al(n * d * el), al(w.kpad ? d * kpad * 2 : 0)};
+  for (int i = 0; i < 11; ++i) {
+    w.sz[i] = sz[i];
+    w.total += sz[i];
+  }
+  w.ao_w = ao_rows * d / n;   // >= d, and >= 6 n_mels for Whisper (two im2col frames per token)
+  w.hw = hw;
+  return w;
+}
+
+void bind_workspace(eas_encoder* e, char* base, const WsPlan& w) {
+  char* p = base;
+  e->x = (float*)p; p += w.sz[0];
+  e->stats = (float2*)p; p += w.sz[1];
+  e->qkv = p; p += w.sz[2];
+  e->ao = p; p += w.sz[3];
+  e->hbuf = p; p += w.sz[4];
+  e->pos3 = (int4*)p; p += w.sz[5];
+  e->tab_idx = (int*)p; p += w.sz[6];
+  e->sinus = (float*)p; p += w.sz[7];
+  const int64_t half = e->cfg.hidden / e->cfg.heads / 2;
+  e->inv_freq = (float*)p;
+  e->slot_axis = (int*)(p + (half * 4 + 255) / 256 * 256);
+  p += w.sz[8];
+  e->xn = p; p += w.sz[9];
+  e->kpad = w.kpad;
+  e->patch_w = w.kpad ? p : nullptr;
+  e->ao_w = w.ao_w;
+  e->hw = w.hw;
+}
+
+// Whisper's sinusoid table and the rotary slot tables, computed on the device.
+hipError_t init_tables(eas_encoder* e, hipStream_t s) {
+  const eas_config& c = e->cfg;
+  if (c.kind == EAS_KIND_WHISPER) return launch_sinusoid_table(e->sinus, c.n_frames / 2, c.hidden, s);
+  if (c.kind == EAS_KIND_VIT_ROPE) return launch_rope_table(e->inv_freq, e->slot_axis, c.rope_sections, c.rope_theta, s);
+  return hipSuccess;
+}
 
 eas_status fail(eas_encoder* e, eas_status s, const std::string& msg) {
   if (e) e->err = msg;
@@ -624,6 +697,69 @@ int split_point(const eas_encoder* e, const int32_t* cu, int n, int64_t* in_off,
   return 0;
 }
 
+// The Encode pass of one checked micro-batch on handle enc (a created
+// handle, or a view over the scratch array), on stream s.
+eas_status encode_call(eas_encoder* enc, const void* packed_in, const int32_t* cu_seqlens, const int32_t* grid_thw,
+                       int32_t n_seqs, const void* weights, void* out_embeddings, int32_t* cu_out, hipStream_t s) {
+  const eas_config& c = enc->cfg;
+  if (c.kind == EAS_KIND_VIT_CLS_ABS && c.layers == 0 && c.out_dtype != EAS_FP32)
+    return fail(enc, EAS_ERR_UNSUPPORTED, "zero-layer CLS model needs fp32 output");
+  eas_status rc = EAS_OK;
+  if (enc->kpad) {   // the zero-padded patch weight, shared by both halves of a split call
+    const int K = (int)k_patch(c), kp = enc->kpad, d = c.hidden;
+    rc = run(enc, s, 0.0, (double)d * (K + kp) * 2, [&](const char** kn) {
+      *kn = "pad_cols";
+      return launch_pad_cols16(wptr(weights, enc, "patch.w"), d, K, kp, enc->patch_w, s);
+    });
+    if (rc != EAS_OK) return rc;
+  }
+  int64_t in_off = 0, out_off = 0;
+  const int k = split_point(enc, cu_seqlens, n_seqs, &in_off, &out_off);
+  if (k == 0) {
+    rc = encode_part(enc, enc->rows_from(0), packed_in, cu_seqlens, grid_thw, n_seqs, weights, out_embeddings, s);
+  } else {
+    // requests [0, k) on the caller's stream and [k, n) on the encoder's second
+    // stream, forked from the caller's stream and joined back into it
+    std::vector<int32_t> cub(n_seqs - k + 1);
+    for (int r = 0; r <= n_seqs - k; ++r) cub[r] = cu_seqlens[k + r] - cu_seqlens[k];
+    if (hipEventRecord(enc->ev_fork, s) != hipSuccess || hipStreamWaitEvent(enc->side, enc->ev_fork, 0) != hipSuccess)
+      return fail(enc, EAS_ERR_HIP, "stream fork failed");
+    rc = encode_part(enc, enc->rows_from(0), packed_in, cu_seqlens, grid_thw, k, weights, out_embeddings, s);
+    if (rc == EAS_OK)
+      rc = encode_part(enc, enc->rows_from(cu_seqlens[k]), static_cast<const char*>(packed_in) + in_off, cub.data(),
+                       grid_thw ? grid_thw + 3 * k : nullptr, n_seqs - k, weights,
+                       static_cast<char*>(out_embeddings) + out_off, enc->side);
+    // joined even after an error: the caller's stream never runs ahead of the side stream
+    const bool joined = hipEventRecord(enc->ev_join, enc->side) == hipSuccess &&
+                        hipStreamWaitEvent(s, enc->ev_join, 0) == hipSuccess;
+    if (rc == EAS_OK && !joined) rc = fail(enc, EAS_ERR_HIP, "stream join failed");
+  }
+  if (enc->ev_done && hipEventRecord(enc->ev_done, s) != hipSuccess && rc == EAS_OK)
+    rc = fail(enc, EAS_ERR_HIP, "event record failed");
+  if (rc != EAS_OK) return rc;
+  if (cu_out) {
+    for (int r = 0; r <= n_seqs; ++r) cu_out[r] = c.merge == 2 ? cu_seqlens[r] / 4 : cu_seqlens[r];
+  }
+  enc->err.clear();
+  return EAS_OK;
+}
+
+// Device address of this device's scratch array, looked up once per device
+// (with that device current) and kept; NULL if the lookup fails.
+char* scratch_base(int dev) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static char* base[kMaxDevices] = {};
+  if (dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!base[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return nullptr;
+    base[dev] = static_cast<char*>(p);
+  }
+  return base[dev];
+}
+
 }  // namespace
 
 extern "C" {
@@ -711,70 +847,16 @@ eas_status eas_encoder_create(const eas_config* cfg, eas_encoder** out) {
     delete e;
     return EAS_ERR_HIP;
   }
-  const eas_config& c = *cfg;
-  const int64_t N = c.max_tokens, d = c.hidden, el = c.dtype == EAS_BF16 ? 2 : 4;
-  const int64_t hw = std::max<int64_t>({c.mlp, 4 * d, 3 * d});
-  int64_t qkv_rows = N, ao_rows = N;
-  if (c.kind == EAS_KIND_WHISPER) {   // front-end im2col and conv1 output reuse qkv / ao
-    qkv_rows = std::max<int64_t>(N, (2 * N * d + 3 * d - 1) / (3 * d));
-    ao_rows = std::max<int64_t>(N, (2 * N * 3 * c.n_mels + d - 1) / d);
-  }
-  auto al = [](int64_t b) { return (b + 255) / 256 * 256; };
-  const int64_t half = d / c.heads / 2;
-  // bf16 ViTs whose patch row is not a whole number of 64-element k-tiles run the
-  // embedding GEMM on zero-padded copies (rows in hbuf, weight in patch_w)
-  const int64_t kp = k_patch(c), kpad = (kp + 63) / 64 * 64;
-  if (c.dtype == EAS_BF16 && c.kind != EAS_KIND_WHISPER && kp % 64 && kpad <= hw) e->kpad = (int)kpad;
-  int64_t sz[11] = {al(N * d * 4), al(N * 8), al(qkv_rows * 3 * d * el), al(ao_rows * d * el), al(N * hw * el),
-                    al(N * 16), al(N * 4), al(c.kind == EAS_KIND_WHISPER ? (int64_t)c.n_frames / 2 * d * 4 : 256),
-                    al(half * 8 + 256), al(N * d * el), al(e->kpad ? d * kpad * 2 : 0)};
-  int64_t total = 0;
-  for (int64_t v : sz) total += v;
-  if (hipMalloc(&e->ws, total) != hipSuccess) {
+  const WsPlan plan = plan_workspace(*cfg, cfg->max_tokens);
+  if (hipMalloc(&e->ws, plan.total) != hipSuccess) {
     delete e;
     return EAS_ERR_HIP;
   }
-  char* p = e->ws;
-  e->x = (float*)p; p += sz[0];
-  e->stats = (float2*)p; p += sz[1];
-  e->qkv = p; p += sz[2];
-  e->ao = p; p += sz[3];
-  e->hbuf = p; p += sz[4];
-  e->pos3 = (int4*)p; p += sz[5];
-  e->tab_idx = (int*)p; p += sz[6];
-  e->sinus = (float*)p; p += sz[7];
-  e->inv_freq = (float*)p;
-  e->slot_axis = (int*)(p + al(half * 4));
-  p += sz[8];
-  e->xn = p;
-  p += sz[9];
-  if (e->kpad) e->patch_w = p;
-  e->ao_w = ao_rows * d / N;   // >= d, and >= 6 n_mels for Whisper (two im2col frames per token)
-  e->hw = hw;
-  hipError_t herr = hipSuccess;
-  if (c.kind == EAS_KIND_WHISPER) {   // Whisper-style sinusoid table, computed in double
-    const int64_t F = c.n_frames / 2, hc = d / 2;
-    std::vector<float> tab(F * d);
-    const double inc = std::log(10000.0) / (double)(hc - 1);
-    for (int64_t t = 0; t < F; ++t)
-      for (int64_t i = 0; i < hc; ++i) {
-        const double a = (double)t * std::exp(-inc * (double)i);
-        tab[t * d + i] = (float)std::sin(a);
-        tab[t * d + hc + i] = (float)std::cos(a);
-      }
-    herr = hipMemcpy(e->sinus, tab.data(), tab.size() * 4, hipMemcpyHostToDevice);
-  }
-  if (c.kind == EAS_KIND_VIT_ROPE && herr == hipSuccess) {   // slot k of axis a turns by theta^(-j / n_a)
-    std::vector<float> inv;
-    std::vector<int> ax;
-    for (int a = 0; a < 3; ++a)
-      for (int j = 0; j < c.rope_sections[a]; ++j) {
-        inv.push_back((float)std::pow((double)c.rope_theta, -(double)j / (double)c.rope_sections[a]));
-        ax.push_back(a);
-      }
-    herr = hipMemcpy(e->inv_freq, inv.data(), inv.size() * 4, hipMemcpyHostToDevice);
-    if (herr == hipSuccess) herr = hipMemcpy(e->slot_axis, ax.data(), ax.size() * 4, hipMemcpyHostToDevice);
-  }
+  bind_workspace(e, e->ws, plan);
+  const eas_config& c = *cfg;
+  // the position tables, once, on the null stream
+  hipError_t herr = init_tables(e, nullptr);
+  if (herr == hipSuccess) herr = hipStreamSynchronize(nullptr);
   // second stream and fork / join events for split micro-batches (default
   // priority); without them every call runs as one pass
   if (herr == hipSuccess && c.max_seqs >= 2) {
@@ -904,54 +986,40 @@ eas_status eas_encode_microbatch(eas_encoder* enc, const void* packed_in, const 
                                  int32_t* cu_out, void* stream) {
   if (!enc) return EAS_ERR_INVALID_ARG;
   if (!packed_in || !weights || !out_embeddings) return fail(enc, EAS_ERR_INVALID_ARG, "NULL device pointer");
-  const eas_config& c = enc->cfg;
   eas_status st;
-  const std::string why = check_batch(c, cu_seqlens, grid_thw, n_seqs, &st);
+  const std::string why = check_batch(enc->cfg, cu_seqlens, grid_thw, n_seqs, &st);
   if (st != EAS_OK) return fail(enc, st, why);
-  if (c.kind == EAS_KIND_VIT_CLS_ABS && c.layers == 0 && c.out_dtype != EAS_FP32)
-    return fail(enc, EAS_ERR_UNSUPPORTED, "zero-layer CLS model needs fp32 output");
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess || dev != enc->device)
     return fail(enc, EAS_ERR_INVALID_ARG, "current device differs from the handle's device");
+  return encode_call(enc, packed_in, cu_seqlens, grid_thw, n_seqs, weights, out_embeddings, cu_out,
+                     static_cast<hipStream_t>(stream));
+}
 
+eas_status eas_encode_microbatch_noalloc(const eas_config* cfg, const void* packed_in, const int32_t* cu_seqlens,
+                                         const int32_t* grid_thw, int32_t n_seqs, const void* weights,
+                                         void* out_embeddings, int32_t* cu_out, void* stream) {
+  if (!cfg || !packed_in || !weights || !out_embeddings) return EAS_ERR_INVALID_ARG;
+  eas_status st;
+  if (!check_config(*cfg, &st).empty()) return st;
+  check_batch(*cfg, cu_seqlens, grid_thw, n_seqs, &st);
+  if (st != EAS_OK) return st;
+  const WsPlan plan = plan_workspace(*cfg, cu_seqlens[n_seqs]);
+  if (plan.total > (int64_t)EAS_NOALLOC_SCRATCH_BYTES) return EAS_ERR_CAPACITY;
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return EAS_ERR_HIP;
+  char* base = scratch_base(dev);
+  if (!base) return EAS_ERR_HIP;
+  // a handle on the host stack over this device's scratch array: no second
+  // stream (the micro-batch runs as one pass), no profiling, no events
+  eas_encoder view;
+  view.cfg = *cfg;
+  view.layout = build_layout(*cfg);
+  view.device = dev;
+  bind_workspace(&view, base, plan);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  eas_status rc = EAS_OK;
-  if (enc->kpad) {   // the zero-padded patch weight, shared by both halves of a split call
-    const int K = (int)k_patch(c), kp = enc->kpad, d = c.hidden;
-    rc = run(enc, s, 0.0, (double)d * (K + kp) * 2, [&](const char** kn) {
-      *kn = "pad_cols";
-      return launch_pad_cols16(wptr(weights, enc, "patch.w"), d, K, kp, enc->patch_w, s);
-    });
-    if (rc != EAS_OK) return rc;
-  }
-  int64_t in_off = 0, out_off = 0;
-  const int k = split_point(enc, cu_seqlens, n_seqs, &in_off, &out_off);
-  if (k == 0) {
-    rc = encode_part(enc, enc->rows_from(0), packed_in, cu_seqlens, grid_thw, n_seqs, weights, out_embeddings, s);
-  } else {
-    // requests [0, k) on the caller's stream and [k, n) on the encoder's second
-    // stream, forked from the caller's stream and joined back into it
-    std::vector<int32_t> cub(n_seqs - k + 1);
-    for (int r = 0; r <= n_seqs - k; ++r) cub[r] = cu_seqlens[k + r] - cu_seqlens[k];
-    if (hipEventRecord(enc->ev_fork, s) != hipSuccess || hipStreamWaitEvent(enc->side, enc->ev_fork, 0) != hipSuccess)
-      return fail(enc, EAS_ERR_HIP, "stream fork failed");
-    rc = encode_part(enc, enc->rows_from(0), packed_in, cu_seqlens, grid_thw, k, weights, out_embeddings, s);
-    if (rc == EAS_OK)
-      rc = encode_part(enc, enc->rows_from(cu_seqlens[k]), static_cast<const char*>(packed_in) + in_off, cub.data(),
-                       grid_thw ? grid_thw + 3 * k : nullptr, n_seqs - k, weights,
-                       static_cast<char*>(out_embeddings) + out_off, enc->side);
-    // joined even after an error: the caller's stream never runs ahead of the side stream
-    const bool joined = hipEventRecord(enc->ev_join, enc->side) == hipSuccess &&
-                        hipStreamWaitEvent(s, enc->ev_join, 0) == hipSuccess;
-    if (rc == EAS_OK && !joined) rc = fail(enc, EAS_ERR_HIP, "stream join failed");
-  }
-  if (hipEventRecord(enc->ev_done, s) != hipSuccess && rc == EAS_OK) rc = fail(enc, EAS_ERR_HIP, "event record failed");
-  if (rc != EAS_OK) return rc;
-  if (cu_out) {
-    for (int r = 0; r <= n_seqs; ++r) cu_out[r] = c.merge == 2 ? cu_seqlens[r] / 4 : cu_seqlens[r];
-  }
-  enc->err.clear();
-  return EAS_OK;
+  if (init_tables(&view, s) != hipSuccess) return EAS_ERR_HIP;
+  return encode_call(&view, packed_in, cu_seqlens, grid_thw, n_seqs, weights, out_embeddings, cu_out, s);
 }
 
 }  // extern "C"

@@ -373,6 +373,50 @@ inline unsigned blocks_for(long n, int bs) { return (unsigned)((n + bs - 1) / bs
 
 }  // namespace
 
+namespace {
+
+// Whisper-style sinusoid table [F, d]: columns i < d/2 hold sin(t * w_i) and
+// columns d/2 + i hold cos(t * w_i), w_i = exp(-i ln(10^4) / (d/2 - 1));
+// evaluated in double, stored as fp32.
+__global__ void sinusoid_table_kernel(float* tab, int F, int d) {
+  const int hc = d / 2;
+  const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (long)F * hc) return;
+  const int t = (int)(idx / hc), i = (int)(idx % hc);
+  const double a = (double)t * exp(-log(10000.0) / (double)(hc - 1) * (double)i);
+  tab[(long)t * d + i] = (float)sin(a);
+  tab[(long)t * d + hc + i] = (float)cos(a);
+}
+
+// Rotary slot tables: the sections s0, s1, s2 of slots turn with the t, h
+// and w position; slot j of an axis with n slots turns by theta^(-j / n).
+__global__ void rope_table_kernel(float* inv_freq, int* slot_axis, int s0, int s1, int s2, float theta) {
+  const int k = threadIdx.x;
+  if (k >= s0 + s1 + s2) return;
+  const int ax = k < s0 ? 0 : (k < s0 + s1 ? 1 : 2);
+  const int j = k - (ax == 0 ? 0 : (ax == 1 ? s0 : s0 + s1));
+  const int n = ax == 0 ? s0 : (ax == 1 ? s1 : s2);
+  inv_freq[k] = (float)pow((double)theta, -(double)j / (double)n);
+  slot_axis[k] = ax;
+}
+
+}  // namespace
+
+hipError_t launch_sinusoid_table(float* tab, int F, int d, hipStream_t s) {
+  if (d < 4 || d % 2) return hipErrorInvalidValue;
+  const long total = (long)F * (d / 2);
+  if (total == 0) return hipSuccess;
+  hipLaunchKernelGGL(sinusoid_table_kernel, dim3(blocks_for(total, 256)), dim3(256), 0, s, tab, F, d);
+  return hipGetLastError();
+}
+
+hipError_t launch_rope_table(float* inv_freq, int* slot_axis, const int sections[3], float theta, hipStream_t s) {
+  if (sections[0] + sections[1] + sections[2] > 256) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(rope_table_kernel, dim3(1), dim3(256), 0, s, inv_freq, slot_axis, sections[0], sections[1],
+                     sections[2], theta);
+  return hipGetLastError();
+}
+
 hipError_t launch_positions(const SeqMeta& m, int N, int4* pos3, int* tab_idx, int pos_gw, hipStream_t s) {
   hipLaunchKernelGGL(positions_kernel, dim3(blocks_for(N, 256)), dim3(256), 0, s, m, N, pos3, tab_idx, pos_gw);
   return hipGetLastError();

@@ -45,7 +45,8 @@ class KernelStat(ctypes.Structure):
 
 EXPORTS = ("eas_encoder_create", "eas_encoder_destroy", "eas_weights_layout", "eas_microbatch_shape",
            "eas_validate_microbatch", "eas_pack_microbatch", "eas_encode_microbatch", "eas_profile_enable",
-           "eas_profile_read", "eas_status_string", "eas_last_error")
+           "eas_profile_read", "eas_status_string", "eas_last_error", "eas_encode_microbatch_noalloc")
+EAS_NOALLOC_SCRATCH_BYTES = 256 << 20
 
 
 def _load():
@@ -65,6 +66,7 @@ def _load():
         "eas_profile_read": ([VP, P(KernelStat), I32, P(I32)], I32),
         "eas_status_string": ([I32], ctypes.c_char_p),
         "eas_last_error": ([VP], ctypes.c_char_p),
+        "eas_encode_microbatch_noalloc": ([P(Config), VP, P(I32), P(I32), I32, VP, VP, P(I32), VP], I32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -165,6 +167,22 @@ def upload_weights(cfg, weights, device="cuda"):
 def _stream_ptr(stream):
     s = stream if stream is not None else torch.cuda.current_stream()
     return ctypes.c_void_p(s.cuda_stream)
+
+
+def encode_microbatch_noalloc(cfg, packed, cu_seqlens, grid_thw, weights, out, stream=None):
+    """eas_encode_microbatch_noalloc: the Encode pass with no handle and no
+    allocation (workspace in the library's fixed per-device array).  ``out``
+    is the caller's [rows, out_dim] tensor.  Returns cu_out."""
+    cu, pcu = _i32(cu_seqlens)
+    pg = None
+    if grid_thw is not None:
+        g, pg = _i32(grid_thw)
+    n = len(cu) - 1
+    cu_out, pco = _i32(np.zeros(n + 1))
+    _check(LIB.eas_encode_microbatch_noalloc(ctypes.byref(cfg), ctypes.c_void_p(packed.data_ptr()), pcu, pg, n,
+                                             ctypes.c_void_p(weights.data_ptr()), ctypes.c_void_p(out.data_ptr()),
+                                             pco, _stream_ptr(stream)))
+    return cu_out
 
 
 class Encoder:
