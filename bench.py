@@ -128,7 +128,7 @@ class Workload:
         self.weights_host = synth.make_weights(preset, seed)
         self.items_host = synth.make_items(preset, pool, seed)
         self.gen_s = time.time() - t0
-        cfg = eas.make_config(preset, 1 << 30, 1)
+        cfg = eas.make_config(preset, 1 << 18, 1)   # shape queries only
         tchw = [list(a.shape) if a.ndim == 4 else [1, 1] + list(a.shape) for a in self.items_host]
         self.item_tokens = [int(eas.microbatch_shape(cfg, [t])[0][-1]) for t in tchw]
         max_tokens = sum(sorted(self.item_tokens)[-max_batch:])

@@ -813,10 +813,13 @@ hipError_t launch_gemm_bf16(const GemmArgs& a, hipStream_t s, const char** kname
     *kname = "gemm_bf16_64x128";
     return launch_tile<64, 128, 2, 2, 3>(a, s);
   }
-  if (async_res_ok(a) && best_tile(a.M, a.N, nullptr) == 0) {
-    *kname = "gemm_bf16_async_res_256x256";   // 8 waves of 64 x 128: 4 KB fp32 slabs
-    return launch_async_t<256, 256, 4, 2, 1, 1>(a, s);
-  }
+  if (async_res_ok(a)) switch (best_tile(a.M, a.N, nullptr)) {
+      case 0:
+        *kname = "gemm_bf16_async_res_256x256";   // 8 waves of 64 x 128: 4 KB fp32 slabs
+        return launch_async_t<256, 256, 4, 2, 1, 1>(a, s);
+      case 1: *kname = "gemm_bf16_async_res_256x128"; return launch_async_t<256, 128, 4, 2, 1, 1>(a, s);
+      default: *kname = "gemm_bf16_async_res_128x128"; return launch_async_t<128, 128, 2, 2, 1, 1>(a, s);
+    }
   if (async_ok(a)) switch (best_tile(a.M, a.N, nullptr)) {
       case 0:   // 16 waves of 64 x 64 with bf16 output (2 KB slabs); the fp32 slabs need 8 waves
         *kname = "gemm_bf16_async_256x256";
