@@ -7,7 +7,7 @@ eas_encode_microbatch).  The headline workload is a micro-batch of 64 CLIP
 ViT-L/14-336 images (577 tokens each, bf16 weights N(0, 0.02), pixels U[0,1),
 seed 0), the image workload of the paper's Table 3.  Prints ONE JSON line.
 
-Besides the headline, every workload of the evaluation (section 5.1) is swept
+Besides the headline, every workload of the evaluation (Section 4.1) is swept
 over micro-batch sizes on a fixed pool of requests: a pass walks the whole
 pool in consecutive micro-batches of size B, so every B encodes the same
 requests (CLIP: 64 images; variable-resolution Qwen2-VL-style images: 64
@@ -344,8 +344,8 @@ def serving(wl, rows, load, live_s, B=64, p=0.6, max_age=1.0):
 
     * replay cost of the library's batcher per arrival (C++);
     * four dispatch policies on one Poisson trace (the comparison of the
-      paper's Figure 4), and the Poisson-gap rule under Gamma arrivals of CV
-      0.5, 1, 2 (Section 5's sensitivity study), through a single encode
+      paper's Figure 5), and the Poisson-gap rule under Gamma arrivals of CV
+      0.5, 1, 2 (Section 4.5's sensitivity study), through a single encode
       server that takes the measured micro-batch times;
     * a live replay: Poisson arrivals at the same load drive the GPU encoder
       in real time; latency = batch completion (HIP event) - arrival."""

@@ -27,7 +27,13 @@
 extern "C" {
 #endif
 
-/* Holds n_cus compute units (1 <= n_cus <= the device's CU count) from the
+/* Largest n_cus eas_cu_reserve accepts on a device of device_cus compute
+ * units: all but one CU per shader engine (gfx950 has 8 CUs per shader
+ * engine, so 224 of MI355X's 256).  Host only, no HIP calls; 0 for
+ * device_cus <= 0. */
+int32_t eas_cu_reserve_max(int32_t device_cus);
+
+/* Holds n_cus compute units (1 <= n_cus <= eas_cu_reserve_max(CU count)) from the
  * moment the kernel enqueued on `stream` (hipStream_t as void*) starts until
  * *release != 0 or max_seconds (0 < max_seconds <= 60) have passed, whichever
  * comes first; every workgroup exits by the time limit at the latest.
@@ -42,9 +48,9 @@ extern "C" {
  *     and streams sharing a queue run in order: work on a stream that shares
  *     `stream`'s queue waits for the reservation to end.  Keep the streams in
  *     use fewer than GPU_MAX_HW_QUEUES (set before HIP starts).
- *   - Leave at least one free CU per shader engine (32 CUs on MI355X): with
+ *   - At least one CU per shader engine stays free (32 CUs on MI355X): with
  *     fewer, some shader engine has none, and other kernels stall behind it
- *     until the reservation ends.
+ *     until the reservation ends; a larger n_cus is refused.
  * Returns EAS_ERR_INVALID_ARG for NULL pointers or out-of-range sizes, and
  * EAS_ERR_HIP if the launch fails. */
 eas_status eas_cu_reserve(int32_t n_cus, double max_seconds, int32_t* started, const int32_t* release, void* stream);

@@ -87,16 +87,20 @@ typedef struct {
   int64_t shape[2];
 } eas_tensor_desc;
 
-/* Validates *cfg and allocates the workspace for cfg->max_tokens tokens and
+/* Not from the paper (library plumbing): the handle of one encoder.
+ * Validates *cfg and allocates the workspace for cfg->max_tokens tokens and
  * cfg->max_seqs requests on the current device.  *out receives the handle.
  * Errors: INVALID_ARG (NULL, inconsistent fields), UNSUPPORTED (a head_dim or
  * width the kernels are not built for), HIP (allocation failed). */
 eas_status eas_encoder_create(const eas_config* cfg, eas_encoder** out);
 
-/* Waits for the handle's pending work and frees its workspace.  NULL-safe. */
+/* Not from the paper (library plumbing).  Waits for the handle's own pending
+ * work -- its last eas_encode_microbatch call on the caller's stream and its
+ * second stream, not the whole device -- and frees its workspace.  NULL-safe. */
 void eas_encoder_destroy(eas_encoder* enc);
 
-/* Canonical layout of the flat weight buffer for *cfg: one descriptor per
+/* Not from the paper (the paper names the encoders but not their weights).
+ * Canonical layout of the flat weight buffer for *cfg: one descriptor per
  * tensor, in order -- the embedding (patch.w [hidden, C*tp*p*p] and patch.b,
  * or conv1.w [hidden, n_mels*3], conv1.b, conv2.w [hidden, hidden*3],
  * conv2.b, both flattened in (channel, tap) order), then cls, pos and
@@ -109,7 +113,8 @@ void eas_encoder_destroy(eas_encoder* enc);
 eas_status eas_weights_layout(const eas_config* cfg, eas_tensor_desc* descs, int32_t capacity,
                               int32_t* n_descs, int64_t* total_bytes);
 
-/* Shape of a micro-batch before it is packed (host only, no HIP calls).
+/* Not from the paper (shape rules of the packed format below).
+ * Shape of a micro-batch before it is packed (host only, no HIP calls).
  * tchw: host [n_req, 4] = (frames, channels, height, width) per request; for
  * WHISPER (1, 1, n_mels, n_frames).  Writes cu_seqlens (host [n_req+1]: the
  * prefix sums of the per-request token counts, a CLS token included),
@@ -119,7 +124,8 @@ eas_status eas_microbatch_shape(const eas_config* cfg, int32_t n_req, const int3
                                 int32_t* cu_seqlens, int32_t* grid_thw, int64_t* packed_elems,
                                 int64_t* out_rows);
 
-/* Checks a packed micro-batch description against *cfg (host only, no HIP
+/* Not from the paper (argument checking).
+ * Checks a packed micro-batch description against *cfg (host only, no HIP
  * calls): 1 <= n_seqs <= max_seqs, cu_seqlens[0] == 0, strictly increasing,
  * cu_seqlens[n_seqs] <= max_tokens; per request the token count matches its
  * grid (t*h*w, +1 for the CLS token; n_frames/2 for WHISPER), h and w are even
@@ -128,7 +134,9 @@ eas_status eas_microbatch_shape(const eas_config* cfg, int32_t n_req, const int3
 eas_status eas_validate_microbatch(const eas_config* cfg, const int32_t* cu_seqlens,
                                    const int32_t* grid_thw, int32_t n_seqs);
 
-/* Micro-batch packer: concatenates requests without padding.
+/* Micro-batch packer (Section 3.2: the encode worker runs a micro-batch of
+ * up to B queued requests as one encoder pass): concatenates requests
+ * without padding.
  * items: host array of n_req device pointers to fp32 inputs -- images and
  * clips [frames, C, H, W], audio [n_mels, n_frames]; tchw as in
  * eas_microbatch_shape.  packed (device, cfg->dtype): vision [N, C*tp*p*p]
@@ -143,7 +151,10 @@ eas_status eas_pack_microbatch(eas_encoder* enc, int32_t n_req, const float* con
                                const int32_t* tchw, void* packed, int32_t* cu_seqlens,
                                int32_t* grid_thw, void* stream);
 
-/* The Encode forward pass on one packed micro-batch (Section 2.1, 3.2).
+/* The Encode forward pass on one packed micro-batch: the encoder and
+ * connector that turn a request's raw input into the embeddings the LLM
+ * consumes (Section 2.1), run on one micro-batch (Section 3.2); each
+ * request's rows leave as one contiguous block (Section 3.3).
  * packed_in (device, cfg->dtype): as written by eas_pack_microbatch.
  * cu_seqlens (host [n_seqs+1]), grid_thw (host [n_seqs, 3]; NULL for WHISPER).
  * weights (device): flat buffer laid out by eas_weights_layout.
@@ -186,8 +197,8 @@ eas_status eas_encode_microbatch_noalloc(const eas_config* cfg, const void* pack
                                          const int32_t* grid_thw, int32_t n_seqs, const void* weights,
                                          void* out_embeddings, int32_t* cu_out, void* stream);
 
-/* Kernel timing for measurement.  While enabled, every launch the handle makes
- * is bracketed by HIP events on its stream.  eas_profile_read waits for the
+/* Not from the paper (measurement).  Kernel timing: while enabled, every
+ * launch the handle makes is bracketed by HIP events on its stream.  eas_profile_read waits for the
  * recorded events and returns, per kernel, the number of launches, the summed
  * event time (ms), and the summed algorithmic flops and HBM bytes of those
  * launches; it then clears the record.  Pass stats == NULL to query the count. */

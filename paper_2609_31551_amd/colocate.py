@@ -29,9 +29,16 @@ import time
 
 from .eas import LIB, EAS_OK, EasError
 
-EXPORTS = ("eas_cu_reserve",)
+EXPORTS = ("eas_cu_reserve", "eas_cu_reserve_max")
 LIB.eas_cu_reserve.argtypes = [ctypes.c_int32, ctypes.c_double, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
 LIB.eas_cu_reserve.restype = ctypes.c_int32
+LIB.eas_cu_reserve_max.argtypes = [ctypes.c_int32]
+LIB.eas_cu_reserve_max.restype = ctypes.c_int32
+
+
+def reserve_max(device_cus):
+    """Largest share eas_cu_reserve accepts: all but one CU per shader engine."""
+    return int(LIB.eas_cu_reserve_max(int(device_cus)))
 
 LEVELS = (0.125, 0.3, 0.5, 0.7, 0.9)   # allocation levels profiled (fractions of the device's CUs)
 THRESHOLD = 0.2                      # latency within 20% of exclusive access counts as safe

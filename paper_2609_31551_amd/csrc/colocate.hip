@@ -35,6 +35,15 @@ __global__ __launch_bounds__(kHoldThreads) void hold_cu_kernel(int* started, con
 }  // namespace
 }  // namespace eas
 
+// gfx950 groups its compute units into shader engines of 8 (32 on a 256-CU
+// MI355X); a share that leaves some shader engine without a free CU stalls
+// every other kernel behind it, so the reservation keeps one per engine free.
+constexpr int kCusPerShaderEngine = 8;
+
+extern "C" int32_t eas_cu_reserve_max(int32_t device_cus) {
+  return device_cus <= 0 ? 0 : device_cus - (device_cus + kCusPerShaderEngine - 1) / kCusPerShaderEngine;
+}
+
 extern "C" eas_status eas_cu_reserve(int32_t n_cus, double max_seconds, int32_t* started, const int32_t* release,
                                      void* stream) {
   if (!started || !release || !(max_seconds > 0.0) || max_seconds > 60.0) return EAS_ERR_INVALID_ARG;
@@ -43,7 +52,7 @@ extern "C" eas_status eas_cu_reserve(int32_t n_cus, double max_seconds, int32_t*
       hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
       hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess || khz <= 0)
     return EAS_ERR_HIP;
-  if (n_cus < 1 || n_cus > cus) return EAS_ERR_INVALID_ARG;
+  if (n_cus < 1 || n_cus > eas_cu_reserve_max(cus)) return EAS_ERR_INVALID_ARG;
   static bool attr = false;
   if (!attr) {
     if (hipFuncSetAttribute((const void*)eas::hold_cu_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,

@@ -13,7 +13,9 @@ import torch
 from . import configs as C
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libeas.so")
+# EAS_LIBRARY names another build of the same sources (the host-sanitized test
+# build); by default the in-tree library
+LIB_PATH = os.environ.get("EAS_LIBRARY") or os.path.join(_HERE, "libeas.so")
 
 EAS_OK, EAS_ERR_INVALID_ARG, EAS_ERR_SHAPE, EAS_ERR_CAPACITY, EAS_ERR_UNSUPPORTED, EAS_ERR_HIP = range(6)
 EAS_MAX_SEQS = 64

@@ -168,7 +168,7 @@ def arrival_trace(n, rate, cv=1.0, seed=0):
     """n request arrival times (seconds, from 0) with i.i.d. Gamma
     inter-arrival gaps of mean 1/rate and coefficient of variation cv
     (cv = 1: Poisson arrivals).  The arrival patterns of the sensitivity
-    study (Section 5) use cv 0.5, 1 and 2."""
+    study (Section 4.5, Table 7) use cv 0.5, 1 and 2."""
     rng = np.random.Generator(np.random.PCG64(seed + 2))
     shape = 1.0 / (cv * cv)
     gaps = rng.gamma(shape, 1.0 / (rate * shape), size=n)

@@ -135,8 +135,20 @@ def test_every_router_symbol_is_exported():
 def test_every_colocation_symbol_is_exported():
     from paper_2609_31551_amd import colocate
     text = open(os.path.join(ROOT, "include", "eas_colocate.h")).read()
-    names = sorted(set(re.findall(r"^\s*(?:eas_status|void)\s+(eas_\w+)\s*\(", text, re.M)))
-    assert names == ["eas_cu_reserve"]
+    names = sorted(set(re.findall(r"^\s*(?:eas_status|void|int32_t)\s+(eas_\w+)\s*\(", text, re.M)))
+    assert names == ["eas_cu_reserve", "eas_cu_reserve_max"]
     for n in names:
         assert hasattr(eas.LIB, n), n
     assert list(colocate.EXPORTS) == names
+
+
+def test_cu_reservation_keeps_one_cu_per_shader_engine_free():
+    """gfx950 has shader engines of 8 CUs: a reservation may take all but one
+    CU of each (224 of MI355X's 256), and larger shares are refused."""
+    from paper_2609_31551_amd import colocate
+    assert colocate.reserve_max(256) == 224
+    assert colocate.reserve_max(304) == 266
+    assert colocate.reserve_max(8) == 7 and colocate.reserve_max(1) == 0 and colocate.reserve_max(0) == 0
+    assert colocate.reserve_max(-5) == 0
+    # the profile's smallest encode share (12.5%) reserves exactly the limit
+    assert 256 - round(colocate.LEVELS[0] * 256) == colocate.reserve_max(256)

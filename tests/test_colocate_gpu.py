@@ -79,6 +79,6 @@ def test_reservation_refuses_sizes_outside_the_device():
     from paper_2609_31551_amd import eas
     started = torch.zeros(K.device_cus() + 1, dtype=torch.int32, pin_memory=True)
     release = torch.zeros(1, dtype=torch.int32, pin_memory=True)
-    for n in (0, -1, K.device_cus() + 1):
+    for n in (0, -1, K.reserve_max(K.device_cus()) + 1, K.device_cus() + 1):
         assert K.LIB.eas_cu_reserve(n, 1.0, started.data_ptr(), release.data_ptr(), None) == eas.EAS_ERR_INVALID_ARG
     assert int(started.sum()) == 0
