@@ -84,6 +84,9 @@ TRAFFIC_SOURCES = {
     "gemm_bf16_128x128": ("gemm_bf16.hip", "common.h", "eas_api.cpp"),
     "gemm_bf16_async_256x256": ("gemm_bf16.hip", "common.h", "eas_api.cpp"),
     "gemm_bf16_async_res_256x256": ("gemm_bf16.hip", "common.h", "eas_api.cpp"),
+    "gemm_bf16_async_res_256x128": ("gemm_bf16.hip", "common.h", "eas_api.cpp"),
+    "gemm_bf16_async_res_128x128": ("gemm_bf16.hip", "common.h", "eas_api.cpp"),
+    "gemm_bf16_async_256x128": ("gemm_bf16.hip", "common.h", "eas_api.cpp"),
     "gemm_bf16_async_128x128": ("gemm_bf16.hip", "common.h", "eas_api.cpp"),
     "gemm_bf16_64x64": ("gemm_bf16.hip", "common.h", "eas_api.cpp"),
     "gemm_bf16_64x128": ("gemm_bf16.hip", "common.h", "eas_api.cpp"),
@@ -217,10 +220,13 @@ def sweep_rows(wl, sizes, reps, profile):
 
 
 def kernel_table(prof, passes):
-    """Per-kernel time per pass, share, and TFLOP/s (MFMA kernels) or GB/s."""
+    """Per-kernel time per pass, share, algorithmic bytes and flops per launch,
+    and TFLOP/s (MFMA kernels) or GB/s."""
     total_ms = sum(v["ms"] for v in prof.values())
     return {k: {"ms_per_step": v["ms"] / passes, "share": v["ms"] / total_ms,
                 "launches_per_step": v["launches"] / passes,
+                "alg_bytes_per_launch": v["bytes"] / v["launches"],
+                "alg_flops_per_launch": v["flops"] / v["launches"],
                 "tflops" if k.startswith(MFMA_KERNELS) else "gbs":
                     (v["flops"] / (v["ms"] * 1e-3) / 1e12) if k.startswith(MFMA_KERNELS)
                     else (v["bytes"] / (v["ms"] * 1e-3) / 1e9)}
