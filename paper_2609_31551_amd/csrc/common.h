@@ -93,10 +93,59 @@ struct GemmArgs {
   const int* pos_idx; int pos_period;         // table row: pos_idx[m] or m % pos_period
   const float* resid; int ldr;                // fp32 residual (may alias out)
   void* out; int ldo; int out_f32;
+  // Rotary positions applied in the epilogue of the bf16 q | k | v projection
+  // (rope_pos set): output columns [0, rope_cols) are the q and k heads, rope_hd
+  // columns each, in interleaved order -- column 2i of a head holds its x_i and
+  // column 2i + 1 its x_{i + rope_hd/2} -- so each rotated pair sits in adjacent
+  // columns of one lane.  Their weight rows are read from the natural order
+  // (rope_src_row) and the bias is passed already interleaved; q . k is the
+  // same in either order since q and k share it.  Slots [0, rope_sec0) turn
+  // with the t position, the next rope_sec1 with h, the rest with w; rope_c[a]
+  // = -log2(theta) / (slots of axis a).
+  const int4* rope_pos;            // (t, h, w) per output row, or null
+  int rope_hd, rope_cols, rope_sec0, rope_sec1;
+  unsigned rope_hd_inv;            // ceil(2^32 / rope_hd): n / rope_hd = umulhi(n, rope_hd_inv) for n < 2^16
+  float rope_c[3];
 };
+
+// Column n's offset within its head (n < 2^16, hd <= 128: the product's error
+// n * (ceil(2^32/hd) - 2^32/hd) / 2^32 < 2^-16 stays below the 1/hd gap to the
+// next integer, so the quotient is exact).
+__device__ __forceinline__ int rope_in_head(int n, int hd, unsigned hd_inv) {
+  return n - (int)__umulhi((unsigned)n, hd_inv) * hd;
+}
+// Weight row of output column n of an interleaved rotary projection.
+__device__ __forceinline__ int rope_src_row(int n, int hd, unsigned hd_inv, int cols) {
+  if (n >= cols) return n;
+  const int c = rope_in_head(n, hd, hd_inv);
+  return n - c + (c >> 1) + (c & 1) * (hd >> 1);
+}
+// Turns (angle / 2 pi) of rotation slot i at position (pt, ph, pw):
+// pos_axis * theta^(-j / n_axis) / (2 pi).  Components by value: selecting
+// among the fields of a struct in memory would become an indexed load.
+__device__ __forceinline__ float rope_turns(const GemmArgs& a, int i, int pt, int ph, int pw) {
+  const bool ht = i < a.rope_sec0, hh = !ht && i < a.rope_sec0 + a.rope_sec1;
+  const int j = ht ? i : (hh ? i - a.rope_sec0 : i - a.rope_sec0 - a.rope_sec1);
+  const float c = ht ? a.rope_c[0] : (hh ? a.rope_c[1] : a.rope_c[2]);
+  const int pos = ht ? pt : (hh ? ph : pw);
+  return (float)pos * __builtin_amdgcn_exp2f(fmaf((float)j, c, -2.65149613f));   // 2^(j c - log2(2 pi))
+}
+// (x, y) = (x_i, x_{i+half}) rotated by `turns`: x cos - y sin, y cos + x sin.  The
+// hardware sine and cosine take turns; the fraction (exact) keeps them in range.
+__device__ __forceinline__ void rope_rotate(float& x, float& y, float turns) {
+  const float t = __builtin_amdgcn_fractf(turns);
+  const float cs = __builtin_amdgcn_cosf(t), sn = __builtin_amdgcn_sinf(t);
+  const float xr = fmaf(x, cs, -(y * sn));
+  y = fmaf(y, cs, x * sn);
+  x = xr;
+}
 
 // ---- launchers (each returns hipGetLastError() of its launch) --------------
 hipError_t launch_gemm_bf16(const GemmArgs& a, hipStream_t s, const char** kname);
+inline unsigned rope_hd_inv(int hd) { return (unsigned)((0x100000000ull + (unsigned)hd - 1) / (unsigned)hd); }
+// Whether launch_gemm_bf16 runs these arguments with the rotary epilogue (the
+// DMA kernels' operand and epilogue requirements, bf16 output, head_dim % 8 == 0).
+bool gemm_bf16_rope_ok(const GemmArgs& a);
 // Rows [0, h) of a bf16 GEMM whose last round of 256 x 256 tiles would run
 // mostly empty: launched as whole rounds, rows [h, M) as a second launch with
 // a smaller tile.  0 when one launch is as fast.
@@ -135,6 +184,10 @@ hipError_t launch_rope(void* qkv, int ldqkv, int N, int heads, int hd, int is_bf
 // tables (inverse frequency and axis of each of the sections' slots).
 hipError_t launch_sinusoid_table(float* tab, int F, int d, hipStream_t s);
 hipError_t launch_rope_table(float* inv_freq, int* slot_axis, const int sections[3], float theta, hipStream_t s);
+// The q | k | v biases of `layers` layers (layer l's at src + l * stride elements,
+// 3 * cols / 2 values) into dst [layers, 3 cols / 2], the q and k heads
+// (columns [0, cols)) in the interleaved rotary order; bf16.
+hipError_t launch_rope_bias(const void* src, long stride, int layers, int cols, int hd, void* dst, hipStream_t s);
 hipError_t launch_cls(const SeqMeta& m, float* x, int d, const void* cls, const void* pos0, int w_bf16,
                       hipStream_t s);
 // [rows, k] 16-bit rows copied to [rows, kp] (kp % 8 == 0, dst 16-byte aligned), zero-filled past k.

@@ -271,6 +271,7 @@ struct eas_encoder {
   int* slot_axis = nullptr;  // [head_dim/2]
   int kpad = 0;              // bf16 ViT with a patch row of k_patch % 64 != 0: k_patch rounded up to 64
   void* patch_w = nullptr;   // patch weight [hidden, kpad], zero columns past k_patch (bf16)
+  void* qkv_bias = nullptr;  // bf16 rotary ViT: every layer's q | k | v bias, q and k interleaved [layers, 3d]
   int64_t ao_w = 0, hw = 0;  // elements per token of ao and hbuf
   hipStream_t side = nullptr;                          // second half of a split micro-batch
   hipEvent_t ev_fork = nullptr, ev_join = nullptr;
@@ -292,11 +293,20 @@ namespace {
 // Bytes of each workspace buffer of an encode pass over up to n tokens, in
 // the order bind_workspace lays them out (each 256-byte aligned).
 struct WsPlan {
-  int64_t sz[11];
+  int64_t sz[12];
   int64_t total = 0;
   int64_t ao_w = 0, hw = 0;   // elements per token of ao and hbuf
   int kpad = 0;
+  bool rope = false;          // rotary positions in the q | k | v GEMM's epilogue
 };
+
+// bf16 rotary ViTs rotate q and k in the q | k | v GEMM's epilogue when its
+// operands meet the DMA kernels' requirements (k a whole number of 64-wide
+// steps, head_dim % 8 == 0); the separate rotary pass serves the rest.
+bool rope_in_epilogue(const eas_config& c) {
+  return c.dtype == EAS_BF16 && c.kind == EAS_KIND_VIT_ROPE && c.layers > 0 && c.hidden % 64 == 0 &&
+         c.head_dim % 8 == 0;
+}
 
 WsPlan plan_workspace(const eas_config& c, int64_t n) {
   WsPlan w;
@@ -313,11 +323,13 @@ WsPlan plan_workspace(const eas_config& c, int64_t n) {
   // embedding GEMM on zero-padded copies (rows in hbuf, weight in patch_w)
   const int64_t kp = k_patch(c), kpad = (kp + 63) / 64 * 64;
   if (c.dtype == EAS_BF16 && c.kind != EAS_KIND_WHISPER && kp % 64 && kpad <= hw) w.kpad = (int)kpad;
-  const int64_t sz[11] = {al(n * d * 4), al(n * 8), al(qkv_rows * 3 * d * el), al(ao_rows * d * el),
+  w.rope = rope_in_epilogue(c);
+  const int64_t sz[12] = {al(n * d * 4), al(n * 8), al(qkv_rows * 3 * d * el), al(ao_rows * d * el),
                           al(n * hw * el), al(n * 16), al(n * 4),
                           al(c.kind == EAS_KIND_WHISPER ? (int64_t)c.n_frames / 2 * d * 4 : 256),
-                          al(half * 8 + 256), al(n * d * el), al(w.kpad ? d * kpad * 2 : 0)};
-  for (int i = 0; i < 11; ++i) {
+                          al(half * 8 + 256), al(n * d * el), al(w.kpad ? d * kpad * 2 : 0),
+                          al(w.rope ? (int64_t)c.layers * 3 * d * 2 : 0)};
+  for (int i = 0; i < 12; ++i) {
     w.sz[i] = sz[i];
     w.total += sz[i];
   }
@@ -343,6 +355,8 @@ void bind_workspace(eas_encoder* e, char* base, const WsPlan& w) {
   e->xn = p; p += w.sz[9];
   e->kpad = w.kpad;
   e->patch_w = w.kpad ? p : nullptr;
+  p += w.sz[10];
+  e->qkv_bias = w.rope ? p : nullptr;
   e->ao_w = w.ao_w;
   e->hw = w.hw;
 }
@@ -456,6 +470,13 @@ eas_status ln_gemm(eas_encoder* e, const Workspace& w, GemmArgs g, float eps, in
 const char* wptr(const void* weights, const eas_encoder* e, const std::string& name) {
   const int64_t off = e->layout.off(name);
   return off < 0 ? nullptr : static_cast<const char*>(weights) + off;
+}
+
+// This call rotates q and k in the q | k | v GEMM's epilogue: the handle has
+// the interleaved biases' workspace and the weight rows are 16-byte aligned
+// (every layer's are, as layer 0's: tensors sit at 256-byte offsets).
+bool rope_fused(const eas_encoder* e, const void* weights) {
+  return e->qkv_bias && (uintptr_t)wptr(weights, e, "layers.0.qkv.w") % 16 == 0;
 }
 
 }  // namespace
@@ -590,6 +611,7 @@ eas_status encode_part(eas_encoder* enc, const Workspace& ws, const void* packed
 
   // ---- layers ----
   const int act = c.act == EAS_ACT_GELU ? ACT_GELU : ACT_QUICKGELU;
+  const bool fuse_rope = rope_fused(enc, weights);
   const int mid_f32 = bf ? 0 : 1;   // qkv / attention / MLP activations: model dtype
   for (int l = 0; l < c.layers; ++l) {
     const std::string p = "layers." + std::to_string(l) + ".";
@@ -598,8 +620,19 @@ eas_status encode_part(eas_encoder* enc, const Workspace& ws, const void* packed
     gq.ln_b = W(p + "ln1.b");
     gq.ln_dim = d;
     gq.bias = W(p + "qkv.b");
+    if (fuse_rope) {
+      gq.bias = static_cast<const char*>(enc->qkv_bias) + (size_t)l * d3 * 2;
+      gq.rope_pos = ws.pos3;
+      gq.rope_hd = hd;
+      gq.rope_hd_inv = rope_hd_inv(hd);
+      gq.rope_cols = 2 * d;
+      gq.rope_sec0 = c.rope_sections[0];
+      gq.rope_sec1 = c.rope_sections[1];
+      for (int a = 0; a < 3; ++a)
+        gq.rope_c[a] = c.rope_sections[a] > 0 ? (float)(-std::log2((double)c.rope_theta) / c.rope_sections[a]) : 0.0f;
+    }
     EAS_TRY(ln_gemm(enc, ws, gq, c.ln_eps, 1, s));
-    if (c.kind == EAS_KIND_VIT_ROPE)
+    if (c.kind == EAS_KIND_VIT_ROPE && !fuse_rope)
       EAS_TRY(run(enc, s, 0.0, (double)N * 2 * d * el * 2 + (double)N * 16, [&](const char** kn) {
         *kn = "rope";
         return launch_rope(ws.qkv, d3, N, H, hd, bf, ws.pos3, enc->inv_freq, enc->slot_axis, s);
@@ -710,6 +743,17 @@ eas_status encode_call(eas_encoder* enc, const void* packed_in, const int32_t* c
     rc = run(enc, s, 0.0, (double)d * (K + kp) * 2, [&](const char** kn) {
       *kn = "pad_cols";
       return launch_pad_cols16(wptr(weights, enc, "patch.w"), d, K, kp, enc->patch_w, s);
+    });
+    if (rc != EAS_OK) return rc;
+  }
+  if (rope_fused(enc, weights)) {   // the interleaved q | k | v biases of every layer, shared likewise
+    const int d = c.hidden;
+    const int64_t o0 = enc->layout.off("layers.0.qkv.b");
+    const long stride = c.layers > 1 ? (long)((enc->layout.off("layers.1.qkv.b") - o0) / 2) : 0;
+    rc = run(enc, s, 0.0, (double)c.layers * 3 * d * 4, [&](const char** kn) {
+      *kn = "rope_bias";
+      return launch_rope_bias(static_cast<const char*>(weights) + o0, stride, c.layers, 2 * d, c.head_dim,
+                              enc->qkv_bias, s);
     });
     if (rc != EAS_OK) return rc;
   }

@@ -400,7 +400,27 @@ __global__ void rope_table_kernel(float* inv_freq, int* slot_axis, int s0, int s
   slot_axis[k] = ax;
 }
 
+// dst[l, n] = src[l * stride + rope_src_row(n)]: every layer's q | k | v bias with
+// the q and k heads interleaved for the rotary epilogue.
+__global__ void rope_bias_kernel(const bf16* src, long stride, int w, int cols, int hd, unsigned hd_inv, bf16* dst,
+                                 long total) {
+  const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= total) return;
+  const int l = (int)(idx / w), n = (int)(idx % w);
+  dst[idx] = src[l * stride + rope_src_row(n, hd, hd_inv, cols)];
+}
+
 }  // namespace
+
+hipError_t launch_rope_bias(const void* src, long stride, int layers, int cols, int hd, void* dst, hipStream_t s) {
+  const int w = cols / 2 * 3;
+  const long total = (long)layers * w;
+  if (cols % 2 || hd % 2 || hd > 128 || cols % hd || w >= 65536) return hipErrorInvalidValue;
+  if (total == 0) return hipSuccess;
+  hipLaunchKernelGGL(rope_bias_kernel, dim3(blocks_for(total, 256)), dim3(256), 0, s, static_cast<const bf16*>(src),
+                     stride, w, cols, hd, rope_hd_inv(hd), static_cast<bf16*>(dst), total);
+  return hipGetLastError();
+}
 
 hipError_t launch_sinusoid_table(float* tab, int F, int d, hipStream_t s) {
   if (d < 4 || d % 2) return hipErrorInvalidValue;

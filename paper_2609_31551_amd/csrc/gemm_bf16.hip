@@ -139,7 +139,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_tile_kernel(GemmArgs
 #pragma unroll
     for (int j = 0; j < C::DB; ++j) {
       const int r = (wave * C::DB + j) * C::RPI + rr;
-      const int gn = min(n0 + r, a.N - 1);
+      int gn = min(n0 + r, a.N - 1);
+      if (a.rope_pos) gn = rope_src_row(gn, a.rope_hd, a.rope_hd_inv, a.rope_cols);
       b_off[j] = (unsigned)(((long)gn * a.ldb + (pch ^ C::sw(r)) * 8) * 2);
     }
   }
@@ -282,6 +283,12 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_tile_kernel(GemmArgs
 #pragma unroll
           for (int e = 0; e < 8; ++e) v[e] = quick_gelu(v[e]);
         }
+        if (a.rope_pos && n < a.rope_cols) {   // four interleaved pairs, slots i0 .. i0 + 3
+          const int4 rp = a.rope_pos[m];
+          const int i0 = rope_in_head(n, a.rope_hd, a.rope_hd_inv) >> 1;
+#pragma unroll
+          for (int t = 0; t < 4; ++t) rope_rotate(v[2 * t], v[2 * t + 1], rope_turns(a, i0 + t, rp.x, rp.y, rp.z));
+        }
         if (a.pos) {
           const int pr = a.pos_idx ? a.pos_idx[m] : m % a.pos_period;
           const long pi = (long)pr * a.ld_pos + n;
@@ -349,13 +356,15 @@ struct ACfg : Cfg<BM, BN, WGM, WGN> {
   __device__ static int sw16(int row) { return (row >> 2) & 3; }   // 16-byte chunk swizzle of 64-byte rows
 };
 
-template <int BM, int BN, int WGM, int WGN, int OUTF32, int RES = 0>
+template <int BM, int BN, int WGM, int WGN, int OUTF32, int RES = 0, int ROPE = 0>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_async_kernel(GemmArgs a, int n_tiles) {
   using C = ACfg<BM, BN, WGM, WGN, OUTF32>;
   constexpr int S = C::FM * C::FN * 2 * (OUTF32 ? 2 : 1);   // buffer stores per wave per tile
   constexpr int L = RES ? C::FM * C::FN * 4 : 0;              // residual loads per wave per tile
-  static_assert(C::DPS + S + 1 < 64, "vmcnt range");
+  constexpr int E = 1 + ROPE;                                 // epilogue DMAs per wave per tile (bias, positions)
+  static_assert(C::DPS + S + E < 64, "vmcnt range");
   static_assert(!RES || OUTF32, "the residual stream is fp32");
+  static_assert(!ROPE || (!OUTF32 && C::WM == 64 && C::SLAB >= 2048), "rotary epilogue: bf16 output, 64-row waves");
   extern __shared__ __attribute__((aligned(1024))) char smem[];
   const unsigned lds0 = (unsigned)(size_t)((__attribute__((address_space(3))) char*)smem);
   const int tid = threadIdx.x, lane = tid & 63;
@@ -378,7 +387,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_async_kernel(GemmArg
 #pragma unroll
     for (int j = 0; j < C::DB; ++j) {
       const int r = (wave * C::DB + j) * C::RPI + rr;
-      b_off[j] = (unsigned)(((long)min(n0 + r, a.N - 1) * a.ldb + (pch ^ C::sw(r)) * 8) * 2);
+      int gn = min(n0 + r, a.N - 1);
+      if constexpr (ROPE) gn = rope_src_row(gn, a.rope_hd, a.rope_hd_inv, a.rope_cols);
+      b_off[j] = (unsigned)(((long)gn * a.ldb + (pch ^ C::sw(r)) * 8) * 2);
     }
   };
   auto issue = [&](int kt, int st) {
@@ -398,9 +409,11 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_async_kernel(GemmArg
   char* slab_b = smem + 2 * C::STAGE + wave * C::SLAB;
   float* slab = reinterpret_cast<float*>(slab_b);
   // this wave's WN bias values -> slab bytes [0, 2 WN); the other lanes repeat them
-  auto issue_bias = [&](int n0) {
+  // with the rotary epilogue, the (t, h, w) positions of the wave's 64 rows -> slab bytes [1024, 2048)
+  auto issue_bias = [&](int n0, int m0) {
     const int n = a.bias ? min(n0 + wn * C::WN + (lane % (C::WN / 8)) * 8, a.N - 8) : 0;
     dma16(slab_lds, (unsigned)(n * 2), bias);
+    if constexpr (ROPE) dma16(slab_lds + 1024, (unsigned)(min(m0 + wm * C::WM + lane, a.M - 1) * 16), a.rope_pos);
   };
 
   const int lrow = lane & 31, g = lane >> 5, swz = C::sw(lrow);
@@ -459,7 +472,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_async_kernel(GemmArg
     else if constexpr (RES) wait_vm<(C::DPS + L + S < 63 ? C::DPS + L + S : 63)>();
     else wait_vm<C::DPS + S>();
     __builtin_amdgcn_s_barrier();
-    issue_bias(n0);
+    issue_bias(n0, m0);
 #pragma unroll
     for (int i = 0; i < C::FM; ++i)
 #pragma unroll
@@ -479,8 +492,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_async_kernel(GemmArg
       // k-tile kt+1 has landed; at kt == 0 the previous stores and the bias DMA may follow it
       // (with a residual, k-tile 1 follows the previous epilogue: only the bias DMA)
       if (kt == 0) {
-        if (first || RES) wait_vm<1>();
-        else wait_vm<S + 1>();
+        if (first || RES) wait_vm<E>();
+        else wait_vm<S + E>();
       } else {
         wait_vm<0>();
       }
@@ -555,6 +568,16 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_async_kernel(GemmArg
       for (int j = 0; j < C::FN; ++j)
 #pragma unroll
         for (int q = 0; q < 4; ++q) bq[j][q] = *reinterpret_cast<const uint2*>(slab_b + (j * 32 + 8 * q + 4 * g) * 2);
+      int rpt[ROPE ? C::FM : 1], rph[ROPE ? C::FM : 1], rpw[ROPE ? C::FM : 1];   // the lane's row in each block row
+      if constexpr (ROPE) {
+#pragma unroll
+        for (int i = 0; i < C::FM; ++i) {
+          const int4 p = *reinterpret_cast<const int4*>(slab_b + 1024 + (i * 32 + lrow) * 16);
+          rpt[i] = p.x;
+          rph[i] = p.y;
+          rpw[i] = p.z;
+        }
+      }
       wait_lds();
 #pragma unroll
       for (int i = 0; i < C::FM; ++i) {
@@ -573,6 +596,14 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_async_kernel(GemmArg
             } else if (act == ACT_QUICKGELU) {
 #pragma unroll
               for (int e = 0; e < 4; ++e) v[e] = quick_gelu(v[e]);
+            }
+            if constexpr (ROPE) {   // two interleaved pairs: columns 8q + 4g + (0, 1) and (2, 3)
+              const int n = n0 + wn * C::WN + j * 32 + 8 * q + 4 * g;
+              if (n < a.rope_cols) {
+                const int i0 = rope_in_head(n, a.rope_hd, a.rope_hd_inv) >> 1;
+                rope_rotate(v[0], v[1], rope_turns(a, i0, rpt[i], rph[i], rpw[i]));
+                rope_rotate(v[2], v[3], rope_turns(a, i0 + 1, rpt[i], rph[i], rpw[i]));
+              }
             }
 #pragma unroll
             for (int e = 0; e < 4; ++e) pk.h[e] = (bf16)v[e];
@@ -692,10 +723,10 @@ hipError_t launch_tile(const GemmArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <int BM, int BN, int WGM, int WGN, int OUTF32, int RES = 0>
+template <int BM, int BN, int WGM, int WGN, int OUTF32, int RES = 0, int ROPE = 0>
 hipError_t launch_async_t(const GemmArgs& a, hipStream_t s) {
   using C = ACfg<BM, BN, WGM, WGN, OUTF32>;
-  auto kern = gemm_bf16_async_kernel<BM, BN, WGM, WGN, OUTF32, RES>;
+  auto kern = gemm_bf16_async_kernel<BM, BN, WGM, WGN, OUTF32, RES, ROPE>;
   static int slots = 0;   // co-resident workgroups on this device, found once per instantiation
   if (!slots) {
     hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
@@ -717,6 +748,7 @@ hipError_t launch_async_t(const GemmArgs& a, hipStream_t s) {
 
 template <int BM, int BN, int WGM, int WGN>
 hipError_t launch_async(const GemmArgs& a, hipStream_t s) {
+  if (a.rope_pos) return launch_async_t<BM, BN, WGM, WGN, 0, 0, 1>(a, s);
   return a.out_f32 ? launch_async_t<BM, BN, WGM, WGN, 1>(a, s) : launch_async_t<BM, BN, WGM, WGN, 0>(a, s);
 }
 
@@ -800,7 +832,13 @@ int device_cus() {
   return cus;
 }
 
+bool gemm_bf16_rope_ok(const GemmArgs& a) {
+  return tile_ok(a) && !a.out_f32 && !a.resid && !a.pos && a.rope_hd > 0 && a.rope_hd % 8 == 0 && a.rope_hd <= 128 &&
+         a.rope_hd_inv == rope_hd_inv(a.rope_hd) && a.rope_cols % a.rope_hd == 0 && a.rope_cols <= a.N && a.N < 65536;
+}
+
 hipError_t launch_gemm_bf16(const GemmArgs& a, hipStream_t s, const char** kname) {
+  if (a.rope_pos && !gemm_bf16_rope_ok(a)) return hipErrorInvalidValue;
   if (!tile_ok(a)) return launch_gemm_bf16_staged(a, s, kname);
   // Pick the tile by estimated time.  All tiles sum k in the same order, so
   // the choice never changes a result.
@@ -827,6 +865,7 @@ hipError_t launch_gemm_bf16(const GemmArgs& a, hipStream_t s, const char** kname
   if (async_ok(a)) switch (best_tile(a.M, a.N, nullptr)) {
       case 0:   // 16 waves of 64 x 64 with bf16 output (2 KB slabs); the fp32 slabs need 8 waves
         *kname = "gemm_bf16_async_256x256";
+        if (a.rope_pos) return launch_async_t<256, 256, 4, 4, 0, 0, 1>(a, s);
         return a.out_f32 ? launch_async_t<256, 256, 4, 2, 1>(a, s) : launch_async_t<256, 256, 4, 4, 0>(a, s);
       case 1: *kname = "gemm_bf16_async_256x128"; return launch_async<256, 128, 4, 2>(a, s);
       default: *kname = "gemm_bf16_async_128x128"; return launch_async<128, 128, 2, 2>(a, s);
@@ -860,6 +899,7 @@ GemmArgs gemm_rows(const GemmArgs& a, int m0, int m1) {
   r.out = static_cast<char*>(a.out) + (size_t)m0 * a.ldo * (a.out_f32 ? 4 : 2);
   if (a.resid) r.resid = a.resid + (size_t)m0 * a.ldr;
   if (a.pos_idx) r.pos_idx = a.pos_idx + m0;
+  if (a.rope_pos) r.rope_pos = a.rope_pos + m0;
   return r;
 }
 

@@ -195,8 +195,9 @@ hipError_t launch_cfg(const GemmArgs& a, hipStream_t s) {
 
 hipError_t launch_gemm_bf16_staged(const GemmArgs& a, hipStream_t s, const char** kname) {
   // bf16 models apply LayerNorm in a pass of its own (launch_ln_apply): the
-  // operands here are always bf16 rows
-  if (a.stats) return hipErrorInvalidValue;
+  // operands here are always bf16 rows; the rotary epilogue is the DMA
+  // kernels' alone (its callers fuse it only where they run)
+  if (a.stats || a.rope_pos) return hipErrorInvalidValue;
   const bool aligned = (a.K % BK == 0) && (a.lda % 8 == 0) && (a.ldb % 8 == 0) &&
                        ((uintptr_t)a.A % 16 == 0) && ((uintptr_t)a.B % 16 == 0);
   if (!aligned) {

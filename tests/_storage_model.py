@@ -3,7 +3,9 @@
 Test infrastructure (a diagnostic beside the fp64 reference, not a second
 reference).  The bf16 encoder computes in fp32 but stores its activations in
 bf16 between kernels: the LayerNorm outputs that feed a GEMM, the q / k / v
-rows (again after the rotary step), the softmax probabilities that feed the
+rows (rotary models: q and k once, after the rotary step, where the q | k | v
+GEMM's epilogue rotates them; else again after a separate rotary pass), the
+softmax probabilities that feed the
 P V product, the attention output, the MLP hidden activations, the Whisper
 front end's first convolution and the merger's hidden layer.  The residual
 stream and the embeddings stay fp32.  ``encode`` below is the reference's
@@ -62,6 +64,12 @@ def _embed(cfg, W, packed, cu, grid, rnd):
     return np.concatenate(xs)
 
 
+def rope_in_epilogue(cfg):
+    """The library's rule for rotating q and k in the q | k | v GEMM's
+    epilogue (bf16 rotary models whose GEMM runs whole 64-wide k-steps)."""
+    return cfg["kind"] == O.KIND_VIT_ROPE and cfg["hidden"] % 64 == 0 and cfg["head_dim"] % 8 == 0
+
+
 def encode(cfg, W, packed, cu, grid, rounding=True):
     """(out, cu_out) like ``oracle.encoder.encode``, with bf16 storage points
     when ``rounding`` is true."""
@@ -76,10 +84,15 @@ def encode(cfg, W, packed, cu, grid, rounding=True):
     for i in range(cfg["layers"]):
         p = "layers.%d." % i
         a = rnd(O.layer_norm(x, W[p + "ln1.g"], W[p + "ln1.b"], cfg["ln_eps"]))
-        qkv = rnd(a @ W[p + "qkv.w"].T + W[p + "qkv.b"])
+        qkv = a @ W[p + "qkv.w"].T + W[p + "qkv.b"]
+        fused = ang is not None and rope_in_epilogue(cfg)
+        if not fused:
+            qkv = rnd(qkv)
         q = qkv[:, 0 * d:1 * d].reshape(N, H, hd)
         k = qkv[:, 1 * d:2 * d].reshape(N, H, hd)
         v = qkv[:, 2 * d:3 * d].reshape(N, H, hd)
+        if fused:
+            v = rnd(v)
         if ang is not None:
             q, k = rnd(O.apply_rope(q, ang)), rnd(O.apply_rope(k, ang))
         o = rnd(_attention(q, k, v, cu, rnd).reshape(N, d))
