@@ -92,6 +92,7 @@ TRAFFIC_SOURCES = {
     "gemm_bf16_64x128": ("gemm_bf16.hip", "common.h", "eas_api.cpp"),
     "attn_bf16_hd64": ("attention_dma.hip", "common.h", "eas_api.cpp"),
     "attn_bf16_hd80": ("attention_dma.hip", "common.h", "eas_api.cpp"),
+    "attn_bf16_hd80_q256": ("attention_dma.hip", "common.h", "eas_api.cpp"),
     "ln_apply_bf16": ("elementwise.hip", "common.h", "eas_api.cpp"),
     "rope": ("elementwise.hip", "common.h", "eas_api.cpp"),
 }

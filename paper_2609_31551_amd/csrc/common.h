@@ -29,6 +29,7 @@ struct AttnWork {
   int cu[kMaxSeqs + 1];
   int order[kMaxSeqs];      // order[i] = sequence handled by the i-th tile group
   int tile_start[kMaxSeqs + 1];  // prefix sums of q-tiles over `order`
+  int qt;                   // queries per q-tile
 };
 
 enum Act { ACT_NONE = 0, ACT_GELU = 1, ACT_QUICKGELU = 2 };
@@ -165,9 +166,10 @@ struct AttnArgs {
 };
 hipError_t launch_attention_bf16(const AttnArgs& a, const AttnWork& w, int total_tiles, int N, hipStream_t s,
                                  const char** kname);
-// DMA-fed kernel for head_dim 64 / 80, and its queries per work-list tile
+// DMA-fed kernel for head_dim 64 / 80, and its queries per work-list tile for
+// the sequences of a micro-batch (cu: n + 1 prefix sums)
 bool attention_dma_supported(const AttnArgs& a, int N);
-int attention_dma_q_tile(int hd);
+int attention_dma_q_tile(int hd, const int* cu, int n);
 hipError_t launch_attention_bf16_dma(const AttnArgs& a, const AttnWork& w, int total_tiles, hipStream_t s,
                                      const char** kname);
 hipError_t launch_attention_f32(const AttnArgs& a, const AttnWork& w, int total_tiles, hipStream_t s,

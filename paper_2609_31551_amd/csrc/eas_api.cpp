@@ -523,7 +523,9 @@ eas_status encode_part(eas_encoder* enc, const Workspace& ws, const void* packed
   probe.qkv = ws.qkv;
   probe.ldqkv = 3 * d;
   probe.hd = hd;
-  const int qt = bf && attention_dma_supported(probe, N) ? attention_dma_q_tile(hd) : attention_q_tile(bf);
+  const int qt = bf && attention_dma_supported(probe, N) ? attention_dma_q_tile(hd, cu_seqlens, n_seqs)
+                                                        : attention_q_tile(bf);
+  work.qt = qt;
   int tiles = 0;
   double attn_flops = 0.0;
   for (int i = 0; i < n_seqs; ++i) {
