@@ -375,10 +375,11 @@ hipError_t launch_hd(const AttnArgs& a, const AttnWork& w, int total_tiles, hipS
 
 }  // namespace
 
-// 256-query tiles for head_dim 80 when they add at most 1% query slots over
-// 128-query tiles (video clips: none; a mix of image sizes: usually a few):
-// 4-6% faster on 8192-token clips, 1-2% on a mix of 3600-token images, while
-// for head_dim 64 (577- and 1500-token rows) they measured no faster or slower.
+// 256-query tiles for head_dim 80 when they add at most 2% query slots over
+// 128-query tiles (video clips: none; batches of 32 mixed-size images: 1-2%):
+// on equal slots they measured 4-6% faster (8192-token clips), 3.6% more
+// slots (3600-token images) still 0.5-2.4% faster; for head_dim 64 (577- and
+// 1500-token rows) they measured no faster or slower.
 // Each query's arithmetic does not depend on the tile that holds it, so the
 // choice never changes a result.
 int attention_dma_q_tile(int hd, const int* cu, int n) {
@@ -389,7 +390,7 @@ int attention_dma_q_tile(int hd, const int* cu, int n) {
     s128 += (L + 127) / 128 * 128;
     s256 += (L + 255) / 256 * 256;
   }
-  return s256 * 100 <= s128 * 101 ? 256 : 128;
+  return s256 * 100 <= s128 * 102 ? 256 : 128;
 }
 
 bool attention_dma_supported(const AttnArgs& a, int N) {
