@@ -796,8 +796,13 @@ namespace {
 // a CU); a round of them costs area * slots / 256 / eff in units where a
 // full round of 256 x 256 tiles costs 65536.  A 128 x 128 launch of at most
 // 256 tiles runs one workgroup per CU, at about 0.7 of a shared round.
+// The residual forms (fp32 residual read and written, 8 waves at 256 x 256) lose
+// more on the smaller tiles: against 256 x 256 the 128 x 128 residual kernel
+// measured 0.77-0.81 and the 256 x 128 one 0.69 (video clips' O-projection
+// and FC2, M = 32768, N = 1280, timed back to back at each tile size).
 struct TileOpt { int bm, bn, slots; double eff; };
 constexpr TileOpt kTiles[3] = {{256, 256, 256, 1.00}, {256, 128, 256, 0.80}, {128, 128, 512, 0.90}};
+constexpr TileOpt kTilesRes[3] = {{256, 256, 256, 1.00}, {256, 128, 256, 0.69}, {128, 128, 512, 0.78}};
 
 double tile_time(const TileOpt& o, long M, long N) {
   const long tiles = ((M + o.bm - 1) / o.bm) * ((N + o.bn - 1) / o.bn);
@@ -806,11 +811,12 @@ double tile_time(const TileOpt& o, long M, long N) {
   return (double)((tiles + o.slots - 1) / o.slots) * round;
 }
 
-int best_tile(long M, long N, double* t) {
+int best_tile(long M, long N, double* t, bool res) {
+  const TileOpt* opts = res ? kTilesRes : kTiles;
   int best = 0;
   double best_t = 1e300;
   for (int i = 0; i < 3; ++i) {
-    const double ti = tile_time(kTiles[i], M, N);
+    const double ti = tile_time(opts[i], M, N);
     if (ti < best_t) { best_t = ti; best = i; }
   }
   if (t) *t = best_t;
@@ -855,14 +861,15 @@ hipError_t launch_gemm_bf16(const GemmArgs& a, hipStream_t s, const char** kname
     *kname = "gemm_bf16_64x128";
     return launch_tile<64, 128, 2, 2, 3>(a, s);
   }
-  if (async_res_ok(a)) switch (best_tile(a.M, a.N, nullptr)) {
+  const bool res = a.resid != nullptr;
+  if (async_res_ok(a)) switch (best_tile(a.M, a.N, nullptr, true)) {
       case 0:
         *kname = "gemm_bf16_async_res_256x256";   // 8 waves of 64 x 128: 4 KB fp32 slabs
         return launch_async_t<256, 256, 4, 2, 1, 1>(a, s);
       case 1: *kname = "gemm_bf16_async_res_256x128"; return launch_async_t<256, 128, 4, 2, 1, 1>(a, s);
       default: *kname = "gemm_bf16_async_res_128x128"; return launch_async_t<128, 128, 2, 2, 1, 1>(a, s);
     }
-  if (async_ok(a)) switch (best_tile(a.M, a.N, nullptr)) {
+  if (async_ok(a)) switch (best_tile(a.M, a.N, nullptr, false)) {
       case 0:   // 16 waves of 64 x 64 with bf16 output (2 KB slabs); the fp32 slabs need 8 waves
         *kname = "gemm_bf16_async_256x256";
         if (a.rope_pos) return launch_async_t<256, 256, 4, 4, 0, 0, 1>(a, s);
@@ -870,7 +877,7 @@ hipError_t launch_gemm_bf16(const GemmArgs& a, hipStream_t s, const char** kname
       case 1: *kname = "gemm_bf16_async_256x128"; return launch_async<256, 128, 4, 2>(a, s);
       default: *kname = "gemm_bf16_async_128x128"; return launch_async<128, 128, 2, 2>(a, s);
     }
-  switch (best_tile(a.M, a.N, nullptr)) {
+  switch (best_tile(a.M, a.N, nullptr, res)) {
     case 0: *kname = "gemm_bf16_256x256"; return launch_tile<256, 256, 4, 4>(a, s);
     case 1: *kname = "gemm_bf16_256x128"; return launch_tile<256, 128, 4, 2>(a, s);
     default: *kname = "gemm_bf16_128x128"; return launch_tile<128, 128, 2, 2>(a, s);
@@ -885,9 +892,10 @@ int gemm_bf16_head_rows(const GemmArgs& a) {
   const long head = rounds * 256 / nt * 256;   // rows covered by whole rounds of 256 x 256 tiles
   if (head <= 0 || head >= a.M) return 0;
   if (a.pos && !a.pos_idx && head % a.pos_period) return 0;
+  const bool res = a.resid != nullptr;
   double whole, tail;
-  best_tile(a.M, a.N, &whole);
-  best_tile(a.M - head, a.N, &tail);
+  best_tile(a.M, a.N, &whole, res);
+  best_tile(a.M - head, a.N, &tail, res);
   const double split = tile_time(kTiles[0], head, a.N) + tail;
   return split < 0.97 * whole ? (int)head : 0;
 }
