@@ -86,11 +86,12 @@ __device__ __forceinline__ void decode(const AttnWork& w, int tile, int qt, int*
   *q0 = *s0 + (tile - w.tile_start[i]) * qt;
 }
 
-// head_dim 80 is held to 128 VGPRs (4 waves per SIMD) explicitly: left to
-// itself the register allocator takes 130 and loses a wave per SIMD
+// Held to 128 VGPRs (4 waves per SIMD) explicitly: left to itself the register
+// allocator takes 130 (head_dim 80, and 64 with the staged output) and loses a
+// wave per SIMD
 template <int HD, int QB, int QT>
 __global__ __launch_bounds__(QT / QB * 2)
-__attribute__((amdgpu_waves_per_eu(HD > 64 ? 4 : 1, HD > 64 ? 4 : 8)))
+__attribute__((amdgpu_waves_per_eu(4, HD > 64 ? 4 : 8)))
 void attn_bf16_dma_kernel(AttnArgs a, AttnWork w) {
   using C = AttnCfg<HD, QB, QT>;
   extern __shared__ __attribute__((aligned(1024))) char smem[];
@@ -341,26 +342,41 @@ void attn_bf16_dma_kernel(AttnArgs a, AttnWork w) {
     }
   }
 
+  // Every wave is past the last tile (its reads done): the two K / V buffers now
+  // hold each wave's 32 x HD output block, row-major with the 16-byte chunks of
+  // row r rotated by r, so the stores leave as whole rows (8 rows of a 64-dim
+  // head per instruction) instead of 16-byte pieces of 32 rows.
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  __syncthreads();
   if (!active) return;
+  constexpr int NCH = HD / 8;   // 16-byte chunks per output row
+  static_assert(C::NW * QB * 32 * HD * 2 <= 2 * C::BUF && (32 * NCH) % 64 == 0, "output staging");
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
-    const int qi = qw0 + qb * 32 + l32;
-    if (qi >= s1) continue;
+    char* stg = smem + (wave * QB + qb) * 32 * HD * 2;
     const float inv = C::MFMA_SUM ? 1.0f / o[qb][C::HB - 1][8]
                                   : 1.0f / (l_part[qb] + __shfl_xor(l_part[qb], 32, 64));
-    bf16* out = static_cast<bf16*>(a.out) + (long)qi * a.ldo + h * HD;
 #pragma unroll
     for (int hb = 0; hb < C::HB; ++hb)
 #pragma unroll
       for (int e4 = 0; e4 < 4; ++e4) {
-        const int d = hb * 32 + e4 * 8 + g * 4;
+        const int d = hb * 32 + e4 * 8 + g * 4;   // lanes g = 0, 1 hold the two halves of chunk d / 8
         if (d < HD) {
           union { uint2 u; bf16 h[4]; } st;
 #pragma unroll
           for (int e = 0; e < 4; ++e) st.h[e] = (bf16)(o[qb][hb][e4 * 4 + e] * inv);
-          *reinterpret_cast<uint2*>(out + d) = st.u;
+          *reinterpret_cast<uint2*>(stg + l32 * HD * 2 + (((d >> 3) + l32) % NCH) * 16 + g * 8) = st.u;
         }
       }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // the wave's own writes are visible to it
+    const int qb0 = qw0 + qb * 32;
+#pragma unroll
+    for (int k = 0; k < 32 * NCH / 64; ++k) {
+      const int c = lane + 64 * k, row = c / NCH, ch = c % NCH;
+      const uint4 val = *reinterpret_cast<const uint4*>(stg + row * HD * 2 + ((ch + row) % NCH) * 16);
+      if (qb0 + row < s1)
+        *reinterpret_cast<uint4*>(static_cast<bf16*>(a.out) + (long)(qb0 + row) * a.ldo + h * HD + ch * 8) = val;
+    }
   }
 }
 
