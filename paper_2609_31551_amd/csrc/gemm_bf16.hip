@@ -333,7 +333,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_tile_kernel(GemmArgs
 // A fixed grid of workgroups walks the tile list (block b takes tiles b, b + grid,
 // ...; the same XCD-aware order as above), so a CU moves to its next tile
 // without a relaunch: that tile's k-tile 0 streams in under the last k-step and
-// its k-tile 1 under the epilogue.  The epilogue issues no load the compiler
+// its k-tile 1 right after the epilogue.  The epilogue issues no load the compiler
 // knows of -- the bias row reaches LDS by DMA with the operands -- and writes
 // through buffer stores whose count per wave is fixed (lanes outside the
 // output get an out-of-range offset and are dropped by the buffer unit), so the
@@ -341,9 +341,11 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_tile_kernel(GemmArgs
 // issue order, and the stores keep draining while the next tile's k-loop runs.
 // The MFMA operands are swapped (C^T blocks: each lane holds 4 consecutive
 // columns of one row): with bf16 output the bias and activation are applied in
-// registers and a finished 32 x 32 bf16 block reaches the per-wave staging slab
-// with 8-byte writes (2 KB slabs leave room for 16 waves); fp32 sums go through
-// a 4 KB slab with 16-byte writes.  The products, their order over k and the
+// registers and a finished 32-row block row is staged with 8-byte writes in the
+// LDS stage the last k-tile used (free until the next tile's k-tile 1), so
+// each store instruction writes whole 128-byte rows (+1% against 64-byte half
+// rows through a 2 KB per-wave slab); fp32 sums go through a 4 KB slab with
+// 16-byte writes (a 32-column fp32 row is 128 bytes).  The products, their order over k and the
 // per-element epilogue arithmetic are the same as in the kernel above, so the
 // two kernels give identical bits.
 template <int BM, int BN, int WGM, int WGN, int OUTF32>
@@ -492,7 +494,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_async_kernel(GemmArg
       // k-tile kt+1 has landed; at kt == 0 the previous stores and the bias DMA may follow it
       // (with a residual, k-tile 1 follows the previous epilogue: only the bias DMA)
       if (kt == 0) {
-        if (first || RES) wait_vm<E>();
+        if (first || RES || !OUTF32) wait_vm<E>();
         else wait_vm<S + E>();
       } else {
         wait_vm<0>();
@@ -554,7 +556,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_async_kernel(GemmArg
       else wait_vm<L / (C::FM * C::FN)>();
     }
     __builtin_amdgcn_s_barrier();   // every wave is past the last stage
-    if (!RES && has_next) issue(1, (sb + KT + 1) & 1);
+    if (!RES && OUTF32 && has_next) issue(1, (sb + KT + 1) & 1);
     __builtin_amdgcn_sched_barrier(0);
 
     // ---- epilogue: one 32 x 32 block at a time through the wave's slab ----
@@ -563,30 +565,36 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_async_kernel(GemmArg
     if constexpr (!OUTF32) {
       // bf16 output: bias and activation on the sums in place (columns 8q + 4g + e
       // of each block), then the finished 32 x 32 bf16 block goes through the slab
-      uint2 bq[C::FN][4];
-#pragma unroll
-      for (int j = 0; j < C::FN; ++j)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) bq[j][q] = *reinterpret_cast<const uint2*>(slab_b + (j * 32 + 8 * q + 4 * g) * 2);
-      int rpt[ROPE ? C::FM : 1], rph[ROPE ? C::FM : 1], rpw[ROPE ? C::FM : 1];   // the lane's row in each block row
-      if constexpr (ROPE) {
-#pragma unroll
-        for (int i = 0; i < C::FM; ++i) {
-          const int4 p = *reinterpret_cast<const int4*>(slab_b + 1024 + (i * 32 + lrow) * 16);
-          rpt[i] = p.x;
-          rph[i] = p.y;
-          rpw[i] = p.z;
-        }
-      }
-      wait_lds();
+      // the stage the last k-tile used is free until the next tile's k-tile 1 (DMA'd
+      // after the epilogue): each wave stages a 32 x WN block row there, row-major
+      // with the 16-byte chunks of row r swizzled by r & 7, and stores whole rows
+      constexpr int RS = C::WN * 2, CPRS = C::WN / 8;
+      static_assert(C::NW * 32 * RS <= C::STAGE && (32 * CPRS) % 64 == 0, "bf16 output staging");
+      char* stg = smem + ((sb + KT - 1) & 1) * C::STAGE + wave * 32 * RS;
+      // read-back: lane -> row r0 (+ RST per pass), 16-byte chunk ch; the row's swizzle
+      // r & 7 is r0 & 7 on passes with (k * RST) % 8 == 0 (rd0), else (r0 + RST) & 7 (rd1)
+      constexpr int RST = 64 / CPRS;
+      static_assert(RST == 4 || RST == 8, "rows per read-back pass");
+      const int r0 = lane / CPRS, ch = lane % CPRS;
+      const int rd0 = r0 * RS + ((ch ^ (r0 & 7)) << 4);
+      const int rd1 = r0 * RS + ((ch ^ ((r0 + RST) & 7)) << 4);
+      const int nst = n0 + wn * C::WN + ch * 8;
+      const unsigned st0 = nst < a.N ? (unsigned)(((wm * C::WM + r0) * a.ldo + nst) * 2) : 0x80000000u;
 #pragma unroll
       for (int i = 0; i < C::FM; ++i) {
+        int pt = 0, ph = 0, pw = 0;   // the lane's row position in block row i
+        if constexpr (ROPE) {
+          const int4 p = *reinterpret_cast<const int4*>(slab_b + 1024 + (i * 32 + lrow) * 16);
+          pt = p.x;
+          ph = p.y;
+          pw = p.z;
+        }
 #pragma unroll
         for (int j = 0; j < C::FN; ++j) {
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
             union { uint2 u; bf16 h[4]; } bb, pk;
-            bb.u = bq[j][q];
+            bb.u = *reinterpret_cast<const uint2*>(slab_b + (j * 32 + 8 * q + 4 * g) * 2);
             float v[4];
 #pragma unroll
             for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * q + e] + (float)bb.h[e] * bias_on;
@@ -601,28 +609,31 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_async_kernel(GemmArg
               const int n = n0 + wn * C::WN + j * 32 + 8 * q + 4 * g;
               if (n < a.rope_cols) {
                 const int i0 = rope_in_head(n, a.rope_hd, a.rope_hd_inv) >> 1;
-                rope_rotate(v[0], v[1], rope_turns(a, i0, rpt[i], rph[i], rpw[i]));
-                rope_rotate(v[2], v[3], rope_turns(a, i0 + 1, rpt[i], rph[i], rpw[i]));
+                rope_rotate(v[0], v[1], rope_turns(a, i0, pt, ph, pw));
+                rope_rotate(v[2], v[3], rope_turns(a, i0 + 1, pt, ph, pw));
               }
             }
 #pragma unroll
             for (int e = 0; e < 4; ++e) pk.h[e] = (bf16)v[e];
-            *reinterpret_cast<uint2*>(slab_b + lrow * 64 + ((q ^ C::sw16(lrow)) << 4) + g * 8) = pk.u;
-          }
-          wait_lds();
-          const int n = n0 + wn * C::WN + j * 32 + pc;
-#pragma unroll
-          for (int p = 0; p < 2; ++p) {
-            const int r = p * 16 + prow, mr = wm * C::WM + i * 32 + r;   // row within the tile
-            const u32x4 val = *reinterpret_cast<const u32x4*>(slab_b + r * 64 + (((lane & 3) ^ C::sw16(r)) << 4));
-            // rows past M fall outside the buffer's range; columns past N are sent out of range
-            const unsigned off = n < a.N ? (unsigned)((mr * a.ldo + n) * 2) : 0x80000000u;
-            // non-temporal: the output is not re-read by this kernel, and
-            // keeping it out of the L2's working set leaves the operand
-            // panels there (+2.5% kernel rate on CLIP's QKV / FC1)
-            __builtin_amdgcn_raw_buffer_store_b128(val, out_rsrc, off, 0, kStoreNT);
+            *reinterpret_cast<uint2*>(stg + lrow * RS + (((4 * j + q) ^ (lrow & 7)) << 4) + g * 8) = pk.u;
           }
         }
+        wait_lds();
+#pragma unroll
+        for (int k = 0; k < 32 / RST; ++k) {
+          const u32x4 val = *reinterpret_cast<const u32x4*>(stg + (((k * RST) & 7) ? rd1 : rd0) + k * RST * RS);
+          // rows past M fall outside the buffer's range; columns past N were sent out of range
+          // non-temporal: the output is not re-read by this kernel, and
+          // keeping it out of the L2's working set leaves the operand
+          // panels there (+2.5% kernel rate on CLIP's QKV / FC1)
+          __builtin_amdgcn_raw_buffer_store_b128(val, out_rsrc, st0 + (unsigned)((i * 32 + k * RST) * a.ldo * 2), 0,
+                                                 kStoreNT);
+        }
+        wait_lds();   // the reads are done before the next block row overwrites the staging
+      }
+      if (has_next) {
+        __builtin_amdgcn_s_barrier();   // every wave has read its staging: k-tile 1 may fill the stage
+        issue(1, (sb + KT + 1) & 1);
       }
     } else {
     uint4 bq[C::FN];
