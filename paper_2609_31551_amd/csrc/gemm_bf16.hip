@@ -345,7 +345,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_tile_kernel(GemmArgs
 // LDS stage the last k-tile used (free until the next tile's k-tile 1), so
 // each store instruction writes whole 128-byte rows (+1% against 64-byte half
 // rows through a 2 KB per-wave slab); fp32 sums go through a 4 KB slab with
-// 16-byte writes (a 32-column fp32 row is 128 bytes).  The products, their order over k and the
+// 16-byte writes and leave, like the fp32 residual they add, in instructions of
+// 8 whole 128-byte rows (1-3% against 16 rows of scattered 16-byte pieces).  The products, their order over k and the
 // per-element epilogue arithmetic are the same as in the kernel above, so the
 // two kernels give identical bits.
 template <int BM, int BN, int WGM, int WGN, int OUTF32>
@@ -511,31 +512,32 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_async_kernel(GemmArg
       mma(fa[(NH - 1) & 1], fb[(NH - 1) & 1]);
       interleave();
     }
-    // Residual epilogue: each lane adds 8 fp32 residual values per 16-row pass, two
-    // passes per 32 x 32 block; a block's 4 loads are issued up to kResAhead blocks
-    // ahead (the first block's under the last k-step).  The loads are ordinary buffer
-    // loads, so the compiler waits for them itself: no DMA is issued between them
-    // and their use, so its counts are exact.  Rows past M and columns past N read 0.
-    const int prow = lane >> 2, pc = (lane & 3) * 8;
+    // fp32 epilogue: eight lanes cover a 128-byte row of a 32 x 32 block, 4 columns
+    // each, so every load and store instruction moves 8 whole rows; four 8-row
+    // passes per block.  Residual epilogue: a block's 4 loads are issued up to
+    // kResAhead blocks ahead (the first block's under the last k-step).  The loads
+    // are ordinary buffer loads, so the compiler waits for them itself: no DMA is
+    // issued between them and their use, so its counts are exact.  Rows past M and
+    // columns past N read 0.
+    const int prow = lane >> 3, pc = (lane & 7) * 4;
     const int rows = min(BM, a.M - m0);
     constexpr int NB = C::FM * C::FN, RR = kResAhead + 1;
-    u32x4 rq[RR][2][2];   // [block % RR][pass][half]
+    u32x4 rq[RR][4];   // [block % RR][pass]
     __amdgpu_buffer_rsrc_t res_rsrc;
     if constexpr (RES)
       res_rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(a.resid) + (size_t)m0 * a.ldr, 0,
                                                    rows * a.ldr * 4, 0x00020000);
-    auto rload = [&](int b, u32x4 (&r)[2][2]) {
+    auto rload = [&](int b, u32x4 (&r)[4]) {
       const int i = b / C::FN, j = b % C::FN;
       const int n = n0 + wn * C::WN + j * 32 + pc;
+      // bit 31 set for columns past N (the sign of N - 1 - n), without a select,
+      // which the compiler would turn into a branch around each load; the row step
+      // of a pass is a scalar added to one per-block offset
+      const unsigned off0 = (unsigned)(((wm * C::WM + i * 32 + prow) * a.ldr + n) * 4) |
+                            ((unsigned)(a.N - 1 - n) & 0x80000000u);
 #pragma unroll
-      for (int p = 0; p < 2; ++p) {
-        const int mr = wm * C::WM + i * 32 + p * 16 + prow;
-        // bit 31 set for columns past N (the sign of N - 1 - n), without a select,
-        // which the compiler would turn into a branch around each pair of loads
-        const unsigned off = (unsigned)((mr * a.ldr + n) * 4) | ((unsigned)(a.N - 1 - n) & 0x80000000u);
-        r[p][0] = __builtin_amdgcn_raw_buffer_load_b128(res_rsrc, off, 0, 0);
-        r[p][1] = __builtin_amdgcn_raw_buffer_load_b128(res_rsrc, off + 16, 0, 0);
-      }
+      for (int p = 0; p < 4; ++p)
+        r[p] = __builtin_amdgcn_raw_buffer_load_b128(res_rsrc, off0 + (unsigned)(p * 8 * a.ldr * 4), 0, 0);
     };
     {
       const int st = (sb + KT - 1) & 1;
@@ -636,9 +638,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_async_kernel(GemmArg
         issue(1, (sb + KT + 1) & 1);
       }
     } else {
-    uint4 bq[C::FN];
+    uint2 bq[C::FN];   // the lane's 4 bias values of each block column
 #pragma unroll
-    for (int j = 0; j < C::FN; ++j) bq[j] = *reinterpret_cast<const uint4*>(slab_b + (j * 32 + pc) * 2);
+    for (int j = 0; j < C::FN; ++j) bq[j] = *reinterpret_cast<const uint2*>(slab_b + (j * 32 + pc) * 2);
     wait_lds();
 #pragma unroll
     for (int i = 0; i < C::FM; ++i) {
@@ -660,48 +662,36 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_async_kernel(GemmArg
               make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
         wait_lds();
         const int n = n0 + wn * C::WN + j * 32 + pc;
-        float bv[8];
+        float bv[4];
         {
-          union { uint4 u; bf16 h[8]; } bb;
+          union { uint2 u; bf16 h[4]; } bb;
           bb.u = bq[j];
 #pragma unroll
-          for (int e = 0; e < 8; ++e) bv[e] = (float)bb.h[e] * bias_on;
+          for (int e = 0; e < 4; ++e) bv[e] = (float)bb.h[e] * bias_on;
         }
+        // rows past M fall outside the buffer's range; columns past N are sent out of range
+        const unsigned st0 = n < a.N ? (unsigned)(((wm * C::WM + i * 32 + prow) * a.ldo + n) * 4) : 0x80000000u;
 #pragma unroll
-        for (int p = 0; p < 2; ++p) {
-          const int r = p * 16 + prow, mr = wm * C::WM + i * 32 + r;   // row within the tile
-          const int sw = C::sw(r);
-          const float4 s0 = *reinterpret_cast<const float4*>(slab + r * 32 + (((pc >> 2) ^ sw) << 2));
-          const float4 s1 = *reinterpret_cast<const float4*>(slab + r * 32 + ((((pc >> 2) + 1) ^ sw) << 2));
-          float v[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
+        for (int p = 0; p < 4; ++p) {
+          const int r = p * 8 + prow;   // row within the block
+          const float4 s0 = *reinterpret_cast<const float4*>(slab + r * 32 + (((pc >> 2) ^ C::sw(r)) << 2));
+          float v[4] = {s0.x, s0.y, s0.z, s0.w};
 #pragma unroll
-          for (int e = 0; e < 8; ++e) v[e] += bv[e];
+          for (int e = 0; e < 4; ++e) v[e] += bv[e];
           if (act == ACT_GELU) {
 #pragma unroll
-            for (int e = 0; e < 8; ++e) v[e] = gelu_erf(v[e]);
+            for (int e = 0; e < 4; ++e) v[e] = gelu_erf(v[e]);
           } else if (act == ACT_QUICKGELU) {
 #pragma unroll
-            for (int e = 0; e < 8; ++e) v[e] = quick_gelu(v[e]);
+            for (int e = 0; e < 4; ++e) v[e] = quick_gelu(v[e]);
           }
           if constexpr (RES) {
 #pragma unroll
-            for (int e = 0; e < 8; ++e) v[e] += __uint_as_float(rq[b % RR][p][e >> 2][e & 3]);
+            for (int e = 0; e < 4; ++e) v[e] += __uint_as_float(rq[b % RR][p][e]);
           }
-          // rows past M fall outside the buffer's range; columns past N are sent out of range
-          const unsigned off = n < a.N ? (unsigned)((mr * a.ldo + n) * es) : 0x80000000u;
-          if (OUTF32) {
-            __builtin_amdgcn_raw_buffer_store_b128(
-                (u32x4){__float_as_uint(v[0]), __float_as_uint(v[1]), __float_as_uint(v[2]), __float_as_uint(v[3])},
-                out_rsrc, off, 0, 0);
-            __builtin_amdgcn_raw_buffer_store_b128(
-                (u32x4){__float_as_uint(v[4]), __float_as_uint(v[5]), __float_as_uint(v[6]), __float_as_uint(v[7])},
-                out_rsrc, off + 16, 0, 0);
-          } else {
-            union { u32x4 u; bf16 h[8]; } pk;
-#pragma unroll
-            for (int e = 0; e < 8; ++e) pk.h[e] = (bf16)v[e];
-            __builtin_amdgcn_raw_buffer_store_b128(pk.u, out_rsrc, off, 0, 0);
-          }
+          __builtin_amdgcn_raw_buffer_store_b128(
+              (u32x4){__float_as_uint(v[0]), __float_as_uint(v[1]), __float_as_uint(v[2]), __float_as_uint(v[3])},
+              out_rsrc, st0 + (unsigned)(p * 8 * a.ldo * 4), 0, 0);
         }
       }
     }
