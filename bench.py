@@ -78,6 +78,35 @@ def copy_calibration(mib):
     print(json.dumps({"copy_calibration_bytes_read": n * 4, "copy_calibration_bytes_written": n * 4}))
 
 
+def mfma_power_probe(n=8192, reps=10):
+    """The vendor library's bf16 matmul (torch.matmul -> hipBLASLt) at n^3 on
+    normally distributed operands and on all-zero operands.  Same instructions,
+    same memory traffic; only the operand bits differ, so the gap is what the
+    board's power budget takes from MFMA throughput when the bits toggle."""
+    import torch
+    g = torch.Generator(device="cuda").manual_seed(7)
+    a = torch.randn(n, n, device="cuda", dtype=torch.bfloat16, generator=g)
+    b = torch.randn(n, n, device="cuda", dtype=torch.bfloat16, generator=g)
+    za, zb = torch.zeros_like(a), torch.zeros_like(b)
+    out = {}
+    for name, x, y in (("random", a, b), ("zero", za, zb)):
+        for _ in range(3):
+            torch.matmul(x, y)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            torch.matmul(x, y)
+        e1.record()
+        torch.cuda.synchronize()
+        out[name + "_tflops"] = 2.0 * n ** 3 * reps / (e0.elapsed_time(e1) * 1e-3) / 1e12
+    out["op"] = "torch.matmul bf16 %d x %d x %d, %d launches back to back" % (n, n, n, reps)
+    out["zero_over_random"] = out["zero_tflops"] / out["random_tflops"]
+    del a, b, za, zb
+    torch.cuda.empty_cache()
+    return out
+
+
 # kernel name -> the sources that decide what it reads and writes per launch
 TRAFFIC_SOURCES = {
     "gemm_bf16_256x256": ("gemm_bf16.hip", "common.h", "eas_api.cpp"),
@@ -521,6 +550,7 @@ def main():
                               "launches_per_step": p["launches"] / args.steps}
         result["kernels"] = kernel_table(prof, args.steps)
         result["gemm_attn_mfma_frac"] = mfma_fraction(prof)
+        result["mfma_power_probe"] = mfma_power_probe()
     workloads = {}
     if sweep:
         workloads[preset["name"]] = {"pool": pool, "sweep": sweep_rows(wl, sweep, args.sweep_steps,
