@@ -94,6 +94,8 @@ struct GemmArgs {
   const int* pos_idx; int pos_period;         // table row: pos_idx[m] or m % pos_period
   const float* resid; int ldr;                // fp32 residual (may alias out)
   void* out; int ldo; int out_f32;
+  int beside;                      // the rows a half leaves after whole rounds of 256 x 256 tiles,
+                                   // launched while the other half's kernels run on another stream
   // Rotary positions applied in the epilogue of the bf16 q | k | v projection
   // (rope_pos set): output columns [0, rope_cols) are the q and k heads, rope_hd
   // columns each, in interleaved order -- column 2i of a head holds its x_i and

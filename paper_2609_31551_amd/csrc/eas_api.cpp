@@ -274,6 +274,7 @@ struct eas_encoder {
   void* qkv_bias = nullptr;  // bf16 rotary ViT: every layer's q | k | v bias, q and k interleaved [layers, 3d]
   int64_t ao_w = 0, hw = 0;  // elements per token of ao and hbuf
   hipStream_t side = nullptr;                          // second half of a split micro-batch
+  bool halves = false;                                 // the call in flight runs as two halves
   hipEvent_t ev_fork = nullptr, ev_join = nullptr;
   hipEvent_t ev_done = nullptr;   // recorded on the caller's stream after each encode call
 
@@ -424,7 +425,9 @@ eas_status gemm(eas_encoder* e, const GemmArgs& g, hipStream_t s) {
     const int h = gemm_bf16_head_rows(g);
     if (h > 0) {
       const eas_status rc = gemm_launch(e, gemm_rows(g, 0, h), s);
-      return rc != EAS_OK ? rc : gemm_launch(e, gemm_rows(g, h, g.M), s);
+      GemmArgs tail = gemm_rows(g, h, g.M);
+      tail.beside = e->halves;
+      return rc != EAS_OK ? rc : gemm_launch(e, tail, s);
     }
   }
   return gemm_launch(e, g, s);
@@ -770,11 +773,13 @@ eas_status encode_call(eas_encoder* enc, const void* packed_in, const int32_t* c
     for (int r = 0; r <= n_seqs - k; ++r) cub[r] = cu_seqlens[k + r] - cu_seqlens[k];
     if (hipEventRecord(enc->ev_fork, s) != hipSuccess || hipStreamWaitEvent(enc->side, enc->ev_fork, 0) != hipSuccess)
       return fail(enc, EAS_ERR_HIP, "stream fork failed");
+    enc->halves = true;
     rc = encode_part(enc, enc->rows_from(0), packed_in, cu_seqlens, grid_thw, k, weights, out_embeddings, s);
     if (rc == EAS_OK)
       rc = encode_part(enc, enc->rows_from(cu_seqlens[k]), static_cast<const char*>(packed_in) + in_off, cub.data(),
                        grid_thw ? grid_thw + 3 * k : nullptr, n_seqs - k, weights,
                        static_cast<char*>(out_embeddings) + out_off, enc->side);
+    enc->halves = false;
     // joined even after an error: the caller's stream never runs ahead of the side stream
     const bool joined = hipEventRecord(enc->ev_join, enc->side) == hipSuccess &&
                         hipStreamWaitEvent(s, enc->ev_join, 0) == hipSuccess;

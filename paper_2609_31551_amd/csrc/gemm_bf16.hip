@@ -853,13 +853,14 @@ hipError_t launch_gemm_bf16(const GemmArgs& a, hipStream_t s, const char** kname
   // smaller tiles multiply the workgroups and three stages keep two k-tiles in
   // flight -- 64 x 128 (4 waves of 32 x 64), or 64 x 64 (4 waves of 32 x 32)
   // while 64 x 128 tiles would leave a quarter of the CUs idle.
-  // A residual launch of at least half a round of 128 x 128 tiles (the rows a
-  // micro-batch half leaves after whole rounds of 256 x 256 tiles) stays on the
-  // persistent residual kernel: it runs beside the other half's kernels, and
-  // measured 1% faster there end to end than the latency tiles (CLIP x64).
+  // The residual rows a micro-batch half leaves after whole rounds of 256 x 256
+  // tiles stay on the persistent residual kernel even when they are few: that
+  // launch runs beside the other half's kernels, and measured 1% faster there
+  // end to end than the latency tiles (CLIP x64).  Alone on the chip (CLIP x4)
+  // the latency tiles are faster.
   const int cus = device_cus();
   const long t128 = (long)((a.M + 127) / 128) * ((a.N + 127) / 128);
-  if (t128 <= cus && !(a.resid && 2 * t128 >= cus && async_res_ok(a))) {
+  if (t128 <= cus && !(a.beside && a.resid && async_res_ok(a))) {
     if ((long)((a.M + 63) / 64) * ((a.N + 127) / 128) * 4 <= 3L * cus) {
       *kname = "gemm_bf16_64x64";
       return launch_tile<64, 64, 2, 2, 3>(a, s);
