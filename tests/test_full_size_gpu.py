@@ -5,11 +5,12 @@ Each test encodes a whole benchmarked micro-batch (the same seeded request
 pools as bench.py) and checks sampled requests against the fp64 reference run
 on that request alone, at full depth where the reference finishes in seconds
 and at two layers otherwise; it also checks that each sampled request's rows
-are bit-identical to its own micro-batch-1 encoding.  At these sizes each
+are bit-identical to its own micro-batch-1 encoding.  From 16384 tokens a
 micro-batch runs as two concurrent halves on two streams, the GEMMs run the
 large-tile path, including the split of quantised grids into a 256 x 256 head
 launch and a smaller-tile tail launch, and attention runs over the longest
-sequences (9216-token images, 8192-token clips).
+sequences (9216-token images, 8192-token clips); the smaller swept sizes (CLIP
+x8, Whisper x8) run in one pass on the persistent kernels' smaller tiles.
 """
 import numpy as np
 import pytest
@@ -41,6 +42,32 @@ def test_clip_microbatch_64_full_depth():
     W = synth.make_weights(p, 0)
     items = synth.make_items(p, 64, 0)
     _check_samples(p, items, W, [5, 63])
+
+
+def test_clip_microbatch_8_full_depth():
+    """The first 8 images of the CLIP pool (4616 tokens, one pass: the residual
+    GEMMs on 128 x 128 persistent tiles), full depth."""
+    p = C.CLIP_L336
+    W = synth.make_weights(p, 0)
+    items = synth.make_items(p, 64, 0)[:8]
+    _check_samples(p, items, W, [0, 7])
+
+
+def test_clip_microbatch_32_full_depth():
+    """The first 32 images of the CLIP pool (18464 tokens: two halves of 16
+    images), full depth."""
+    p = C.CLIP_L336
+    W = synth.make_weights(p, 0)
+    items = synth.make_items(p, 64, 0)[:32]
+    _check_samples(p, items, W, [15, 31])
+
+
+def test_whisper_microbatch_8_full_depth():
+    """The first 8 clips of the audio pool (12000 tokens, one pass), full depth."""
+    p = C.WHISPER_L
+    W = synth.make_weights(p, 0)
+    items = synth.make_items(p, 32, 0)[:8]
+    _check_samples(p, items, W, [7])
 
 
 def test_qwen_image_microbatch_8_full_depth():
