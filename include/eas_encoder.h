@@ -164,7 +164,7 @@ eas_status eas_pack_microbatch(eas_encoder* enc, int32_t n_req, const float* con
  * cu_out (host [n_seqs+1], may be NULL): prefix sums of the output rows.
  * Attention is full within each request and never crosses requests; each
  * request's output does not depend on the other requests in the batch.
- * A micro-batch of 16384 tokens or more (not while profiling) is run as two
+ * A micro-batch of 8192 tokens or more (not while profiling) is run as two
  * halves split by tokens: the first on `stream`, the second on a stream the
  * handle owns, forked from and joined back into `stream` by events, so work
  * enqueued on `stream` afterwards sees the whole result.  Per-request bits do

@@ -709,8 +709,11 @@ eas_status encode_part(eas_encoder* enc, const Workspace& ws, const void* packed
 // within two requests of it whose second-half buffers keep 16-byte alignment
 // (CLIP's 588-element patch rows need an even token offset).  Returns k, or 0
 // for one pass: per-kernel profiling (one stream of events), small batches,
-// and no aligned boundary near the middle.
-constexpr int kSplitTokens = 16384;
+// and no aligned boundary near the middle.  From 8192 tokens: against 16384,
+// CLIP x16 +5.9%, x24 +3.5%, Qwen-style images x4 +1.3%, Whisper x6 +1.0%,
+// Whisper x8 -0.8% (same-box A/B); below it the halves lose (CLIP x4 -4%,
+// Whisper x4 -7% at a 1024-token threshold).
+constexpr int kSplitTokens = 8192;
 int split_point(const eas_encoder* e, const int32_t* cu, int n, int64_t* in_off, int64_t* out_off) {
   const eas_config& c = e->cfg;
   if (e->prof || !e->side || n < 2 || cu[n] < kSplitTokens) return 0;

@@ -5,12 +5,12 @@ Each test encodes a whole benchmarked micro-batch (the same seeded request
 pools as bench.py) and checks sampled requests against the fp64 reference run
 on that request alone, at full depth where the reference finishes in seconds
 and at two layers otherwise; it also checks that each sampled request's rows
-are bit-identical to its own micro-batch-1 encoding.  From 16384 tokens a
+are bit-identical to its own micro-batch-1 encoding.  From 8192 tokens a
 micro-batch runs as two concurrent halves on two streams, the GEMMs run the
 large-tile path, including the split of quantised grids into a 256 x 256 head
 launch and a smaller-tile tail launch, and attention runs over the longest
-sequences (9216-token images, 8192-token clips); the smaller swept sizes (CLIP
-x8, Whisper x8) run in one pass on the persistent kernels' smaller tiles.
+sequences (9216-token images, 8192-token clips); CLIP x8 runs in one pass on
+the persistent kernels' smaller tiles.
 """
 import numpy as np
 import pytest
@@ -63,7 +63,7 @@ def test_clip_microbatch_32_full_depth():
 
 
 def test_whisper_microbatch_8_full_depth():
-    """The first 8 clips of the audio pool (12000 tokens, one pass), full depth."""
+    """The first 8 clips of the audio pool (12000 tokens: two halves), full depth."""
     p = C.WHISPER_L
     W = synth.make_weights(p, 0)
     items = synth.make_items(p, 32, 0)[:8]

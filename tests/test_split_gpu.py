@@ -1,4 +1,4 @@
-"""Micro-batches of 16384 tokens or more run as two concurrent halves, split at a
+"""Micro-batches of 8192 tokens or more run as two concurrent halves, split at a
 request boundary near half the tokens (the second half on the handle's own
 stream).  Every request of such a batch must come out bit-identical to its own
 micro-batch-1 encoding (which runs in one pass), and match the fp64 reference.
@@ -7,7 +7,8 @@ The cases put the boundary where the split logic has choices to make: CLIP with
 29 images (the balanced boundary, after 15 images, would leave the second
 half's patch rows off 16-byte alignment, so the split moves to 14), Qwen images
 with a 256-token second half against 18432 tokens in the first, Whisper with an
-odd clip count, and video at exactly the 16384-token threshold.
+odd clip count, video at 16384 tokens (two clips), and two Qwen images at
+exactly the 8192-token threshold.
 """
 import numpy as np
 import pytest
@@ -23,7 +24,8 @@ CASES = {
     "clip_29": (C.CLIP_L336, 29, None, [0, 14, 28]),
     "qwen_uneven": (C.QWEN_IMAGE, 3, [(2, 1344, 1344), (2, 1344, 1344), (2, 224, 224)], [2]),
     "whisper_11": (C.WHISPER_L, 11, None, [0, 6, 10]),
-    "video_threshold": (C.QWEN_VIDEO, 2, None, []),
+    "video_two_clips": (C.QWEN_VIDEO, 2, None, []),
+    "qwen_threshold": (C.QWEN_IMAGE, 2, [(2, 896, 896), (2, 896, 896)], [1]),
 }
 
 
@@ -34,7 +36,7 @@ def test_split_batch_matches_single_requests_and_reference(case):
     W = synth.make_weights(p, 0)
     items = synth.make_items(p, n, 0, shapes=shapes)
     batch = gpu_encode(p, items, W)
-    assert batch["cu"][-1] >= 16384, batch["cu"][-1]
+    assert batch["cu"][-1] >= 8192, batch["cu"][-1]
     enc, wdev, cu = batch["enc"], batch["wdev"], batch["cu_out"]
     for r in range(n):
         print("[split] %s: request %d of %d alone" % (case, r, n), flush=True)
