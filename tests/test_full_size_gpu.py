@@ -100,6 +100,38 @@ def test_qwen_image_largest_images_two_layers():
     _check_samples(p, items, W, [2])
 
 
+def test_largest_accepted_microbatch_two_layers():
+    """The largest micro-batch a Qwen-style handle accepts (the 32-bit offset
+    cap, 419430 tokens): 45 images of 1344 x 1344 (9216 tokens each) and a
+    224 x 224 one (256 tokens) last, two layers, run as one pass (profiling
+    on, so no split into halves): every launch spans whole buffers, and the
+    last rows of the widest one (FC1's, 5120 columns) end about 1% below 2^31
+    elements.  The small image, at the highest offsets, is checked against the
+    reference and its own single encoding; the last large image against its
+    single encoding."""
+    from paper_2609_31551_amd import eas
+    p = C.with_layers(C.QWEN_IMAGE, 2)
+    W = synth.make_weights(p, 0)
+    shapes = [(2, 1344, 1344)] * 45 + [(2, 224, 224)]
+    items = synth.make_items(p, len(shapes), 0, shapes=shapes)
+    enc = eas.Encoder(p, 419430, max_seqs=len(items))
+    wdev = eas.upload_weights(enc.cfg, W)
+    enc.profile_enable(True)
+    batch = gpu_encode(p, items, W, enc=enc, wdev=wdev)
+    enc.profile_enable(False)
+    enc.profile_read()
+    cu = batch["cu_out"]
+    assert batch["cu"][-1] == 45 * 9216 + 256
+    print("[full-size] largest micro-batch: %d tokens in one pass" % batch["cu"][-1], flush=True)
+    ref = oracle_encode(p, [items[45]], W)
+    e = rel_err(batch["out"][cu[45]:cu[46]], ref["out"])
+    print("[full-size] largest micro-batch: last request relative error %.3g" % e, flush=True)
+    assert e <= TOL[p["dtype"]], e
+    for r in (44, 45):
+        alone = gpu_encode(p, [items[r]], W, enc=enc, wdev=wdev)
+        np.testing.assert_array_equal(alone["out"], batch["out"][cu[r]:cu[r + 1]])
+
+
 def test_video_microbatch_4_two_layers():
     """4 clips of 16 x 448 x 448 (32768 tokens, 8192 per clip), two layers."""
     p = C.with_layers(C.QWEN_VIDEO, 2)
