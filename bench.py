@@ -82,7 +82,8 @@ def mfma_power_probe(n=8192, reps=10):
     """The vendor library's bf16 matmul (torch.matmul -> hipBLASLt) at n^3 on
     normally distributed operands and on all-zero operands.  Same instructions,
     same memory traffic; only the operand bits differ, so the gap is what the
-    board's power budget takes from MFMA throughput when the bits toggle."""
+    board's power budget takes from MFMA throughput when the bits toggle.  Beside
+    it, the library's register-only MFMA probe on random and zero operands."""
     import torch
     g = torch.Generator(device="cuda").manual_seed(7)
     a = torch.randn(n, n, device="cuda", dtype=torch.bfloat16, generator=g)
@@ -102,6 +103,10 @@ def mfma_power_probe(n=8192, reps=10):
         out[name + "_tflops"] = 2.0 * n ** 3 * reps / (e0.elapsed_time(e1) * 1e-3) / 1e12
     out["op"] = "torch.matmul bf16 %d x %d x %d, %d launches back to back" % (n, n, n, reps)
     out["zero_over_random"] = out["zero_tflops"] / out["random_tflops"]
+    # the MFMA issue rate alone: operands in registers, no memory traffic
+    from paper_2609_31551_amd import eas
+    out["register_only_random_tflops"] = eas.mfma_rate_probe(False)
+    out["register_only_zero_tflops"] = eas.mfma_rate_probe(True)
     del a, b, za, zb
     torch.cuda.empty_cache()
     return out

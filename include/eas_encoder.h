@@ -213,6 +213,18 @@ typedef struct {
 eas_status eas_profile_enable(eas_encoder* enc, int32_t enable);
 eas_status eas_profile_read(eas_encoder* enc, eas_kernel_stat* stats, int32_t capacity, int32_t* n_stats);
 
+/* Not from the paper (measurement).  MFMA issue rate with no memory traffic:
+ * one workgroup per CU runs iters x 32 back-to-back v_mfma_f32_32x32x16_bf16 on
+ * operands held in registers -- random finite bf16 values, or all zero when
+ * zero_operands != 0 -- after one warm-up launch, timed with HIP events on
+ * `stream` (synchronised before return).  *tflops: dense bf16 TFLOP/s of the
+ * timed launch.  On random operands the board's power limit, not the clock,
+ * sets the rate; the gap to the zero-operand rate is what the limit takes from
+ * MFMA-bound kernels.  Allocates and frees a small device buffer.  Returns
+ * EAS_ERR_INVALID_ARG for a NULL tflops or iters outside [1, 2^20], EAS_ERR_HIP
+ * on a failed HIP call. */
+eas_status eas_mfma_rate_probe(int32_t zero_operands, int32_t iters, double* tflops, void* stream);
+
 const char* eas_status_string(eas_status s);
 /* Detail of the last failing call on this handle ("" if none; NULL-safe). */
 const char* eas_last_error(const eas_encoder* enc);

@@ -47,7 +47,8 @@ class KernelStat(ctypes.Structure):
 
 EXPORTS = ("eas_encoder_create", "eas_encoder_destroy", "eas_weights_layout", "eas_microbatch_shape",
            "eas_validate_microbatch", "eas_pack_microbatch", "eas_encode_microbatch", "eas_profile_enable",
-           "eas_profile_read", "eas_status_string", "eas_last_error", "eas_encode_microbatch_noalloc")
+           "eas_profile_read", "eas_status_string", "eas_last_error", "eas_encode_microbatch_noalloc",
+           "eas_mfma_rate_probe")
 EAS_NOALLOC_SCRATCH_BYTES = 256 << 20
 
 
@@ -69,6 +70,7 @@ def _load():
         "eas_status_string": ([I32], ctypes.c_char_p),
         "eas_last_error": ([VP], ctypes.c_char_p),
         "eas_encode_microbatch_noalloc": ([P(Config), VP, P(I32), P(I32), I32, VP, VP, P(I32), VP], I32),
+        "eas_mfma_rate_probe": ([I32, I32, P(ctypes.c_double), VP], I32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -169,6 +171,14 @@ def upload_weights(cfg, weights, device="cuda"):
 def _stream_ptr(stream):
     s = stream if stream is not None else torch.cuda.current_stream()
     return ctypes.c_void_p(s.cuda_stream)
+
+
+def mfma_rate_probe(zero_operands=False, iters=50000, stream=None):
+    """Dense bf16 TFLOP/s of back-to-back MFMAs on register-resident random (or
+    all-zero) operands on every CU (eas_mfma_rate_probe; measurement only)."""
+    t = ctypes.c_double()
+    _check(LIB.eas_mfma_rate_probe(1 if zero_operands else 0, int(iters), ctypes.byref(t), _stream_ptr(stream)))
+    return t.value
 
 
 def encode_microbatch_noalloc(cfg, packed, cu_seqlens, grid_thw, weights, out, stream=None):

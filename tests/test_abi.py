@@ -101,6 +101,14 @@ def test_config_errors_are_reported_without_hip():
         eas.microbatch_shape(eas.make_config(C.QWEN_IMAGE, max_tokens=10 ** 5), [[2, 3, 230, 308]])
 
 
+def test_mfma_probe_rejects_bad_arguments_without_hip():
+    import ctypes
+    t = ctypes.c_double()
+    assert eas.LIB.eas_mfma_rate_probe(0, 0, ctypes.byref(t), None) == eas.EAS_ERR_INVALID_ARG
+    assert eas.LIB.eas_mfma_rate_probe(0, (1 << 20) + 1, ctypes.byref(t), None) == eas.EAS_ERR_INVALID_ARG
+    assert eas.LIB.eas_mfma_rate_probe(0, 100, None, None) == eas.EAS_ERR_INVALID_ARG
+
+
 @pytest.mark.parametrize("preset", [C.CLIP_L336, C.QWEN_IMAGE, C.WHISPER_L, C.TINY], ids=lambda p: p["name"])
 def test_max_tokens_is_capped_where_32_bit_offsets_end(preset):
     """A handle's widest per-token buffer (MLP hidden, qkv, merger input,

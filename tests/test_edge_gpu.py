@@ -70,3 +70,15 @@ def test_refused_calls_write_nothing_and_leave_the_handle_usable():
     torch.cuda.synchronize()
     np.testing.assert_array_equal(again_cu, ref_cu)
     np.testing.assert_array_equal(again.cpu().numpy(), ref.numpy())
+
+
+def test_mfma_rate_probe_reports_a_rate_within_the_clock_limit():
+    """The measurement probe's flop count: 256 CUs x 4 SIMDs x one 32x32x16 MFMA
+    (32768 flops) per 32 cycles at 2.4 GHz bound its rate from above; both
+    operand kinds give a positive, finite rate below that bound."""
+    import math
+    from paper_2609_31551_amd import eas
+    for zero in (False, True):
+        print("[edge] mfma rate probe, zero operands=%s" % zero, flush=True)
+        tf = eas.mfma_rate_probe(zero, iters=20000)
+        assert math.isfinite(tf) and 50.0 < tf < 2.62e3, (zero, tf)
