@@ -39,8 +39,28 @@ __global__ void positions_kernel(SeqMeta m, int N, int4* pos3, int* tab_idx, int
 }
 
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  // Butterfly: v += v[lane ^ o] for o = 32, 16, 8, 4, 2, 1, each lane move in
+  // VALU (no LDS round trip): the two swaps pair lanes 32 and 16 apart, a
+  // rotation by 8 within each 16-lane row gives lane ^ 8, shifts by 4 (the one
+  // whose source stays in the row) lane ^ 4, quad permutations lane ^ 2 and
+  // lane ^ 1.  Every lane ends with the same sum, summed in a fixed order.
+  {
+    const auto s = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = __uint_as_float(s[0]) + __uint_as_float(s[1]);
+  }
+  {
+    const auto s = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = __uint_as_float(s[0]) + __uint_as_float(s[1]);
+  }
+  const int lane = __lane_id();
+  v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x128, 0xF, 0xF, false));   // row_ror:8
+  {
+    const int up = __builtin_amdgcn_mov_dpp(__float_as_int(v), 0x104, 0xF, 0xF, false);   // row_shl:4 (lane + 4)
+    const int dn = __builtin_amdgcn_mov_dpp(__float_as_int(v), 0x114, 0xF, 0xF, false);   // row_shr:4 (lane - 4)
+    v += __int_as_float((lane & 4) ? dn : up);
+  }
+  v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x4E, 0xF, 0xF, false));  // quad_perm 2,3,0,1
+  v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0xB1, 0xF, 0xF, false));  // quad_perm 1,0,3,2
   return v;
 }
 
@@ -104,6 +124,17 @@ __global__ __launch_bounds__(256) void ln_apply_vec_kernel(const float* x, int N
   if (row >= N) return;
   const int lane = threadIdx.x & 63, nc = d >> 2;
   const float4* xr = reinterpret_cast<const float4*>(x + (long)row * d);
+  // gamma and beta are fetched with the row, so their latency hides under its
+  // loads and reductions (one LayerNorm over one image's 577 rows is latency-bound)
+  uint2 gv[LNV_MAXC], bv[LNV_MAXC];
+#pragma unroll
+  for (int e = 0; e < LNV_MAXC; ++e) {
+    const int c = lane + 64 * e;
+    if (c < nc) {
+      gv[e] = *reinterpret_cast<const uint2*>(g + 4 * c);
+      bv[e] = *reinterpret_cast<const uint2*>(b + 4 * c);
+    }
+  }
   float4 v[LNV_MAXC];
   float s = 0.0f;
 #pragma unroll
@@ -127,9 +158,12 @@ __global__ __launch_bounds__(256) void ln_apply_vec_kernel(const float* x, int N
     const int c = lane + 64 * e;
     if (c < nc) {
       const float in[4] = {v[e].x, v[e].y, v[e].z, v[e].w};
+      union { uint2 u; W h[4]; } gw, bw;
+      gw.u = gv[e];
+      bw.u = bv[e];
       Y out[4];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) out[j] = (Y)((in[j] - mean) * rstd * (float)g[4 * c + j] + (float)b[4 * c + j]);
+      for (int j = 0; j < 4; ++j) out[j] = (Y)((in[j] - mean) * rstd * (float)gw.h[j] + (float)bw.h[j]);
       if constexpr (sizeof(Y) == 2) {
         union { uint2 u; Y h[4]; } o;
 #pragma unroll
