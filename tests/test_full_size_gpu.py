@@ -62,6 +62,26 @@ def test_clip_microbatch_32_full_depth():
     _check_samples(p, items, W, [15, 31])
 
 
+def test_single_requests_full_depth():
+    """Micro-batch 1 (the low-load end of the sweep), full depth: one CLIP image
+    (577 tokens) and one audio clip (1500 tokens).  Every GEMM then has no more
+    tiles than there are CUs and runs the latency tiles' deep LDS rings; the
+    batched encodings of the same requests (CLIP x8, audio x8) must match them
+    bit for bit."""
+    for p, pool, r in ((C.CLIP_L336, 64, 3), (C.WHISPER_L, 32, 2)):
+        W = synth.make_weights(p, 0)
+        items = synth.make_items(p, pool, 0)[:8]
+        print("[full-size] %s: request %d alone" % (p["name"], r), flush=True)
+        alone = gpu_encode(p, [items[r]], W)
+        ref = oracle_encode(p, [items[r]], W)
+        e = rel_err(alone["out"], ref["out"])
+        print("[full-size] %s: request %d alone, relative error %.3g" % (p["name"], r, e), flush=True)
+        assert e <= TOL[p["dtype"]], (p["name"], e)
+        batch = gpu_encode(p, items, W)
+        cu = batch["cu_out"]
+        np.testing.assert_array_equal(alone["out"], batch["out"][cu[r]:cu[r + 1]])
+
+
 def test_whisper_microbatch_8_full_depth():
     """The first 8 clips of the audio pool (12000 tokens: two halves), full depth."""
     p = C.WHISPER_L
