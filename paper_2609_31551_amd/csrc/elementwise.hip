@@ -126,6 +126,7 @@ __global__ __launch_bounds__(256) void ln_apply_vec_kernel(const float* x, int N
   const float4* xr = reinterpret_cast<const float4*>(x + (long)row * d);
   // gamma and beta are fetched with the row, so their latency hides under its
   // loads and reductions (one LayerNorm over one image's 577 rows is latency-bound)
+  static_assert(sizeof(W) == 2, "gamma / beta fetched as four 16-bit values per 8 bytes");
   uint2 gv[LNV_MAXC], bv[LNV_MAXC];
 #pragma unroll
   for (int e = 0; e < LNV_MAXC; ++e) {
